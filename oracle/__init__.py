@@ -1,0 +1,142 @@
+"""CPU oracle for 3D Deformable Slide Attention (MegaSlide-DiT, Section 5.2, Eq. (1)).
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+bench's CPU-baseline leg may import this package.  It wraps ``dsa3d_oracle.c``
+(plain C, fp64 accumulation, OpenMP) with ctypes and shares nothing with the
+GPU library.  The arithmetic and the readings it follows are described at the
+top of ``dsa3d_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dsa3d_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+
+def build(force: bool = True) -> str:
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11",
+                               _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int64), ("T", ctypes.c_int64), ("H", ctypes.c_int64),
+                ("W", ctypes.c_int64), ("heads", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("kt", ctypes.c_int64), ("kh", ctypes.c_int64), ("kw", ctypes.c_int64),
+                ("scale", ctypes.c_double), ("bf16", ctypes.c_int32), ("pad_", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        vp = ctypes.c_void_p
+        lib.orc_forward.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, vp, ctypes.c_int64, vp, vp]
+        lib.orc_forward.restype = ctypes.c_int
+        lib.orc_backward.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, vp, ctypes.c_int64,
+                                     ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp]
+        lib.orc_backward.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def default_scale(head_dim: int) -> float:
+    """Logit scale 1/sqrt(head_dim) (per-head reading of the paper's 1/sqrt(d))."""
+    return 1.0 / math.sqrt(head_dim)
+
+
+def _problem(shape, dtype: str, scale):
+    B, T, H, W, heads, D, kt, kh, kw = shape
+    if scale is None:
+        scale = default_scale(D)
+    return _Problem(B, T, H, W, heads, D, kt, kh, kw, float(scale), 1 if dtype == "bf16" else 0, 0)
+
+
+def _check_io(a, dtype):
+    want = np.uint16 if dtype == "bf16" else np.float32
+    a = np.ascontiguousarray(a)
+    if a.dtype != want:
+        raise TypeError(f"expected {want} array for dtype {dtype}, got {a.dtype}")
+    return a
+
+
+def forward(shape, dtype, q, k, v, off, rows=None, scale=None):
+    """Attention output and LSE for the given flat query rows (all rows if None).
+
+    shape = (B, T, H, W, heads, head_dim, kt, kh, kw); q/k/v are [B,T,H,W,heads,D]
+    arrays (float32, or uint16 bf16 bit patterns when dtype == "bf16");
+    off is float32 [B,T,H,W,heads,P,3].  Returns (out[nrows, D], lse[nrows]) in fp64.
+    """
+    pr = _problem(shape, dtype, scale)
+    q, k, v = (_check_io(a, dtype) for a in (q, k, v))
+    off = np.ascontiguousarray(off, dtype=np.float32)
+    B, T, H, W, heads, D = shape[:6]
+    if rows is None:
+        rows = np.arange(B * T * H * W * heads, dtype=np.int64)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.empty((rows.size, D), dtype=np.float64)
+    lse = np.empty(rows.size, dtype=np.float64)
+    rc = _load().orc_forward(ctypes.byref(pr), q.ctypes.data, k.ctypes.data, v.ctypes.data,
+                             off.ctypes.data, rows.ctypes.data, rows.size, out.ctypes.data,
+                             lse.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle forward: malformed problem")
+    return out, lse
+
+
+def backward_slab(shape, dtype, q, k, v, off, dout, b, m, t0, t1, scale=None, dk=None, dv=None):
+    """Gradients from the queries of batch b, head m, frames [t0, t1).
+
+    Returns (dq[(t1-t0),H,W,D], doff[(t1-t0),H,W,P,3], dk[T,H,W,D], dv[T,H,W,D]); dk/dv
+    hold only the contributions of those queries (accumulated into the given arrays)."""
+    pr = _problem(shape, dtype, scale)
+    q, k, v, dout = (_check_io(a, dtype) for a in (q, k, v, dout))
+    off = np.ascontiguousarray(off, dtype=np.float32)
+    B, T, H, W, heads, D, kt, kh, kw = shape
+    P = kt * kh * kw
+    dq = np.empty((t1 - t0, H, W, D), dtype=np.float64)
+    doff = np.empty((t1 - t0, H, W, P, 3), dtype=np.float64)
+    if dk is None:
+        dk = np.zeros((T, H, W, D), dtype=np.float64)
+    if dv is None:
+        dv = np.zeros((T, H, W, D), dtype=np.float64)
+    assert dk.flags["C_CONTIGUOUS"] and dv.flags["C_CONTIGUOUS"]
+    rc = _load().orc_backward(ctypes.byref(pr), q.ctypes.data, k.ctypes.data, v.ctypes.data,
+                              off.ctypes.data, dout.ctypes.data, b, m, t0, t1, dq.ctypes.data,
+                              doff.ctypes.data, dk.ctypes.data, dv.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle backward: malformed problem")
+    return dq, doff, dk, dv
+
+
+def backward(shape, dtype, q, k, v, off, dout, scale=None):
+    """Full gradients (dq, dk, dv as [B,T,H,W,heads,D], doff as [B,T,H,W,heads,P,3]), fp64."""
+    B, T, H, W, heads, D, kt, kh, kw = shape
+    P = kt * kh * kw
+    dq = np.empty((B, T, H, W, heads, D))
+    dk = np.empty((B, T, H, W, heads, D))
+    dv = np.empty((B, T, H, W, heads, D))
+    doff = np.empty((B, T, H, W, heads, P, 3))
+    for b in range(B):
+        for m in range(heads):
+            a, o, kk, vv = backward_slab(shape, dtype, q, k, v, off, dout, b, m, 0, T, scale)
+            dq[b, :, :, :, m] = a
+            doff[b, :, :, :, m] = o
+            dk[b, :, :, :, m] = kk
+            dv[b, :, :, :, m] = vv
+    return dq, dk, dv, doff

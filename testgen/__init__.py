@@ -1,0 +1,181 @@
+"""Seeded synthetic inputs for the 3D-DSA parity tests and the bench.
+
+Test infrastructure shared by the oracle side and the GPU side: it only draws
+random numbers (counter-based Philox4x32-10, see ``testgen.c``) and holds none
+of the operator's arithmetic.  The workload table below gives the shapes and
+value distributions of the synthetic video-token grids used throughout.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "testgen.c")
+_LIB = os.path.join(_HERE, "libtestgen.so")
+
+# Tensor ids (part of the counter); fixed so every slab is reproducible.
+TID_Q, TID_K, TID_V, TID_OFF, TID_DOUT = 0, 1, 2, 3, 4
+
+NORMAL, UNIFORM = 0, 1
+
+
+def build(force: bool = True) -> str:
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-shared", "-fPIC", "-std=c11",
+                               _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        lib.tg_fill.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64,
+                                ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                ctypes.c_double, ctypes.c_int, ctypes.c_void_p]
+        lib.tg_fill.restype = None
+        lib.tg_philox4x32_10.argtypes = [ctypes.POINTER(ctypes.c_uint32)] * 3
+        lib.tg_philox4x32_10.restype = None
+        lib.tg_f32_to_bf16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64]
+        lib.tg_f32_to_bf16.restype = None
+        _lib = lib
+    return _lib
+
+
+def philox4x32_10(ctr, key):
+    lib = _load()
+    c = (ctypes.c_uint32 * 4)(*ctr)
+    k = (ctypes.c_uint32 * 2)(*key)
+    o = (ctypes.c_uint32 * 4)()
+    lib.tg_philox4x32_10(c, k, o)
+    return list(o)
+
+
+@dataclasses.dataclass(frozen=True)
+class Dist:
+    kind: int          # NORMAL or UNIFORM
+    a: float           # mean (normal) or low end (uniform)
+    b: float           # std (normal) or high end (uniform)
+    lo: float = -np.inf
+    hi: float = np.inf
+
+
+def fill(out: np.ndarray, seed: int, tid: int, start: int, dist: Dist) -> np.ndarray:
+    """Write elements [start, start + out.size) of tensor `tid` into `out`.
+
+    `out` must be C-contiguous float32 or uint16 (bf16 bit patterns)."""
+    assert out.flags["C_CONTIGUOUS"]
+    if out.dtype == np.float32:
+        bf16 = 0
+    elif out.dtype == np.uint16:
+        bf16 = 1
+    else:
+        raise TypeError("fill: out must be float32 or uint16 (bf16 bits)")
+    _load().tg_fill(seed, tid, start, out.size, dist.kind, dist.a, dist.b, dist.lo, dist.hi, bf16,
+                    out.ctypes.data)
+    return out
+
+
+def f32_to_bf16(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, dtype=np.uint16)
+    _load().tg_f32_to_bf16(x.ctypes.data, out.ctypes.data, x.size)
+    return out
+
+
+def bf16_to_f32(x: np.ndarray) -> np.ndarray:
+    return (x.astype(np.uint32) << 16).view(np.float32)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """A synthetic 3D-DSA problem: grid, heads, kernel, dtype and distributions."""
+    name: str
+    B: int
+    T: int
+    H: int
+    W: int
+    heads: int
+    head_dim: int
+    kt: int
+    kh: int
+    kw: int
+    dtype: str                 # "f32" or "bf16" for q, k, v, out, dout
+    qkv: Dist
+    offsets: Dist
+    seed: int
+    backward: bool
+    dout: Dist = Dist(NORMAL, 0.0, 1.0)
+
+    @property
+    def N(self):
+        return self.T * self.H * self.W
+
+    @property
+    def P(self):
+        return self.kt * self.kh * self.kw
+
+    @property
+    def queries(self):
+        """(token, head) rows."""
+        return self.B * self.N * self.heads
+
+    def qkv_shape(self):
+        return (self.B, self.T, self.H, self.W, self.heads, self.head_dim)
+
+    def off_shape(self):
+        return (self.B, self.T, self.H, self.W, self.heads, self.P, 3)
+
+    def np_io_dtype(self):
+        return np.float32 if self.dtype == "f32" else np.uint16
+
+    def with_grid(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+N01 = Dist(NORMAL, 0.0, 1.0)
+
+WORKLOADS = {
+    # 256 query tokens, fp32, zero-padded borders hit by most points.
+    "tiny_f32": Workload("tiny_f32", 1, 4, 8, 8, 2, 32, 3, 3, 3, "f32", N01,
+                         Dist(NORMAL, 0.0, 0.5), seed=0, backward=False),
+    # 16,384 tokens, bf16 q/k/v, offsets uniform in [-2, 2].
+    "medium_bf16": Workload("medium_bf16", 1, 16, 32, 32, 8, 64, 3, 3, 3, "bf16", N01,
+                            Dist(UNIFORM, -2.0, 2.0), seed=1, backward=False),
+    # 256 frames of a 1080p latent at patch 16: 2,088,960 tokens, 24 heads x 128.
+    "full_1080p_256f": Workload("full_1080p_256f", 1, 256, 68, 120, 24, 128, 3, 3, 3, "bf16", N01,
+                                Dist(NORMAL, 0.0, 1.0, -3.0, 3.0), seed=2, backward=False),
+    # forward + backward, 130,560 tokens, 16 heads x 64.
+    "fwdbwd_64x34x60": Workload("fwdbwd_64x34x60", 1, 64, 34, 60, 16, 64, 3, 3, 3, "bf16", N01,
+                                Dist(UNIFORM, -2.0, 2.0), seed=3, backward=True),
+    # forward + backward, 3x5x5 kernel (75 points), offsets uniform in [-8, 8].
+    "wide_64x68x120_p75": Workload("wide_64x68x120_p75", 1, 64, 68, 120, 24, 128, 3, 5, 5, "bf16",
+                                   N01, Dist(UNIFORM, -8.0, 8.0), seed=4, backward=True),
+}
+
+
+def gen_tensor(w: Workload, tid: int, shape, dist: Dist, io: bool, start: int = 0) -> np.ndarray:
+    out = np.empty(shape, dtype=w.np_io_dtype() if io else np.float32)
+    return fill(out, w.seed, tid, start, dist)
+
+
+def gen_inputs(w: Workload):
+    """Full host copies of q, k, v (io dtype), offsets (fp32) and dout (io dtype)."""
+    q = gen_tensor(w, TID_Q, w.qkv_shape(), w.qkv, True)
+    k = gen_tensor(w, TID_K, w.qkv_shape(), w.qkv, True)
+    v = gen_tensor(w, TID_V, w.qkv_shape(), w.qkv, True)
+    off = gen_tensor(w, TID_OFF, w.off_shape(), w.offsets, False)
+    dout = gen_tensor(w, TID_DOUT, w.qkv_shape(), w.dout, True) if w.backward else None
+    return q, k, v, off, dout
