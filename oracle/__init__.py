@@ -51,8 +51,18 @@ def _load():
         lib.orc_backward.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, vp, ctypes.c_int64,
                                      ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp]
         lib.orc_backward.restype = ctypes.c_int
+        lib.orc_backward_rows.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, vp, vp,
+                                          ctypes.c_int64, vp, vp]
+        lib.orc_backward_rows.restype = ctypes.c_int
+        lib.orc_max_threads.argtypes = []
+        lib.orc_max_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().orc_max_threads())
 
 
 def default_scale(head_dim: int) -> float:
@@ -122,6 +132,24 @@ def backward_slab(shape, dtype, q, k, v, off, dout, b, m, t0, t1, scale=None, dk
     if rc != 0:
         raise ValueError("oracle backward: malformed problem")
     return dq, doff, dk, dv
+
+
+def backward_rows(shape, dtype, q, k, v, off, dout, rows, scale=None):
+    """dq[nrows, D] and doff[nrows, P, 3] (fp64) of the given flat query rows."""
+    pr = _problem(shape, dtype, scale)
+    q, k, v, dout = (_check_io(a, dtype) for a in (q, k, v, dout))
+    off = np.ascontiguousarray(off, dtype=np.float32)
+    D = shape[5]
+    P = shape[6] * shape[7] * shape[8]
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    dq = np.empty((rows.size, D), dtype=np.float64)
+    doff = np.empty((rows.size, P, 3), dtype=np.float64)
+    rc = _load().orc_backward_rows(ctypes.byref(pr), q.ctypes.data, k.ctypes.data, v.ctypes.data,
+                                   off.ctypes.data, dout.ctypes.data, rows.ctypes.data, rows.size,
+                                   dq.ctypes.data, doff.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle backward: malformed problem")
+    return dq, doff
 
 
 def backward(shape, dtype, q, k, v, off, dout, scale=None):

@@ -51,6 +51,7 @@
  * Build: gcc -O2 -fopenmp -shared -fPIC dsa3d_oracle.c -o liboracle.so -lm
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -139,6 +140,17 @@ static void trilinear(const orc_problem* pr, const void* F, const orc_point* s, 
 
 int orc_num_points(const orc_problem* pr) { return (int)(pr->kt * pr->kh * pr->kw); }
 
+/* Threads an OpenMP parallel region of this library uses. */
+int orc_max_threads(void) {
+  int n = 1;
+#pragma omp parallel
+  {
+#pragma omp single
+    n = omp_get_num_threads();
+  }
+  return n;
+}
+
 /*
  * Forward for a list of query rows.
  *   rows[r] = flat index of (b, t, i, j, head), row-major over [B][T][H][W][heads].
@@ -192,6 +204,112 @@ int orc_forward(const orc_problem* pr, const void* q, const void* k, const void*
   return 0;
 }
 
+/* Scratch of one query's backward, sized for P points and D channels. */
+typedef struct {
+  orc_point* pts;
+  double *kp, *vp, *qv, *gv, *sp, *al, *da;
+} orc_scratch;
+
+static void scratch_alloc(orc_scratch* w, int64_t P, int64_t D) {
+  w->pts = (orc_point*)malloc(sizeof(orc_point) * P);
+  w->kp = (double*)malloc(sizeof(double) * D * P);
+  w->vp = (double*)malloc(sizeof(double) * D * P);
+  w->qv = (double*)malloc(sizeof(double) * D);
+  w->gv = (double*)malloc(sizeof(double) * D);
+  w->sp = (double*)malloc(sizeof(double) * P);
+  w->al = (double*)malloc(sizeof(double) * P);
+  w->da = (double*)malloc(sizeof(double) * P);
+}
+
+static void scratch_free(orc_scratch* w) {
+  free(w->pts);
+  free(w->kp);
+  free(w->vp);
+  free(w->qv);
+  free(w->gv);
+  free(w->sp);
+  free(w->al);
+  free(w->da);
+}
+
+/* Backward of one query (b, t, i, j, head m).  Writes dq_out[D] and doff_out[P][3];
+ * when dk/dv are given ([T*H*W][D] of (b, m)) the query's contributions are added there. */
+static void backward_query(const orc_problem* pr, const void* q, const void* k, const void* v,
+                           const float* off, const void* dout, int64_t b, int64_t t, int64_t i,
+                           int64_t j, int64_t m, double* dq_out, double* doff_out, double* dk,
+                           double* dv, orc_scratch* w) {
+  const int64_t P = pr->kt * pr->kh * pr->kw, D = pr->D;
+  const int64_t HW = pr->H * pr->W;
+  const int64_t row = row_of(pr, b, t, i, j, m);
+  for (int64_t d = 0; d < D; ++d) {
+    w->qv[d] = ld(q, pr->bf16, row * D + d);
+    w->gv[d] = ld(dout, pr->bf16, row * D + d);
+  }
+  /* forward recompute */
+  for (int64_t p = 0; p < P; ++p) {
+    sample_point(pr, b, t, i, j, m, p, off + (row * P + p) * 3, &w->pts[p]);
+    trilinear(pr, k, &w->pts[p], w->kp + p * D);
+    trilinear(pr, v, &w->pts[p], w->vp + p * D);
+    double dot = 0.0, dd = 0.0;
+    for (int64_t d = 0; d < D; ++d) {
+      dot += w->qv[d] * w->kp[p * D + d];
+      dd += w->gv[d] * w->vp[p * D + d];
+    }
+    w->sp[p] = pr->scale * dot;
+    w->da[p] = dd;
+  }
+  double mx = -INFINITY;
+  for (int64_t p = 0; p < P; ++p) mx = w->sp[p] > mx ? w->sp[p] : mx;
+  double l = 0.0;
+  for (int64_t p = 0; p < P; ++p) l += exp(w->sp[p] - mx);
+  double delta = 0.0;
+  for (int64_t p = 0; p < P; ++p) {
+    w->al[p] = exp(w->sp[p] - mx) / l;
+    delta += w->al[p] * w->da[p];
+  }
+  /* dq */
+  for (int64_t d = 0; d < D; ++d) {
+    double acc = 0.0;
+    for (int64_t p = 0; p < P; ++p) acc += w->al[p] * (w->da[p] - delta) * w->kp[p * D + d];
+    dq_out[d] = pr->scale * acc;
+  }
+  /* dK, dV scatter and offset gradients */
+  for (int64_t p = 0; p < P; ++p) {
+    const orc_point* s = &w->pts[p];
+    const double al = w->al[p];
+    const double ds = al * (w->da[p] - delta);
+    double g[3] = {0.0, 0.0, 0.0};
+    for (int c = 0; c < 8; ++c) {
+      if (!s->valid[c]) continue;
+      const int cx = c & 1, cy = (c >> 1) & 1, cz = (c >> 2) & 1;
+      const int64_t dst = ((s->crow[c] / pr->heads) % (pr->T * HW)) * D; /* (z,y,x) of batch b */
+      double qk = 0.0, dvv = 0.0;
+      for (int64_t d = 0; d < D; ++d) {
+        const double kc = ld(k, pr->bf16, s->crow[c] * D + d);
+        const double vc = ld(v, pr->bf16, s->crow[c] * D + d);
+        qk += w->qv[d] * kc;
+        dvv += w->gv[d] * vc;
+        if (dk) {
+          const double addk = pr->scale * ds * s->w[c] * w->qv[d];
+          const double addv = al * s->w[c] * w->gv[d];
+#pragma omp atomic
+          dk[dst + d] += addk;
+#pragma omp atomic
+          dv[dst + d] += addv;
+        }
+      }
+      const double G = pr->scale * ds * qk + al * dvv;
+      const double ax[2] = {1.0 - s->frac[0], s->frac[0]};
+      const double ay[2] = {1.0 - s->frac[1], s->frac[1]};
+      const double az[2] = {1.0 - s->frac[2], s->frac[2]};
+      g[0] += G * (cx ? 1.0 : -1.0) * ay[cy] * az[cz];
+      g[1] += G * (cy ? 1.0 : -1.0) * ax[cx] * az[cz];
+      g[2] += G * (cz ? 1.0 : -1.0) * ax[cx] * ay[cy];
+    }
+    for (int a = 0; a < 3; ++a) doff_out[p * 3 + a] = g[a];
+  }
+}
+
 /*
  * Backward for the queries of batch b, head m and frames [t0, t1).
  *   dq   [(t1-t0)*H*W][D]       gradient w.r.t. q of those queries (overwritten)
@@ -209,91 +327,41 @@ int orc_backward(const orc_problem* pr, const void* q, const void* k, const void
   const int64_t nq = (t1 - t0) * HW;
 #pragma omp parallel
   {
-    orc_point* pts = (orc_point*)malloc(sizeof(orc_point) * P);
-    double* kp = (double*)malloc(sizeof(double) * D * P);
-    double* vp = (double*)malloc(sizeof(double) * D * P);
-    double* qv = (double*)malloc(sizeof(double) * D);
-    double* gv = (double*)malloc(sizeof(double) * D);
-    double* sp = (double*)malloc(sizeof(double) * P);
-    double* al = (double*)malloc(sizeof(double) * P);
-    double* da = (double*)malloc(sizeof(double) * P);
+    orc_scratch w;
+    scratch_alloc(&w, P, D);
 #pragma omp for schedule(dynamic, 16)
     for (int64_t n = 0; n < nq; ++n) {
       const int64_t t = t0 + n / HW, i = (n % HW) / pr->W, j = n % pr->W;
-      const int64_t row = row_of(pr, b, t, i, j, m);
-      for (int64_t d = 0; d < D; ++d) {
-        qv[d] = ld(q, pr->bf16, row * D + d);
-        gv[d] = ld(dout, pr->bf16, row * D + d);
-      }
-      /* forward recompute */
-      for (int64_t p = 0; p < P; ++p) {
-        sample_point(pr, b, t, i, j, m, p, off + (row * P + p) * 3, &pts[p]);
-        trilinear(pr, k, &pts[p], kp + p * D);
-        trilinear(pr, v, &pts[p], vp + p * D);
-        double dot = 0.0, dd = 0.0;
-        for (int64_t d = 0; d < D; ++d) {
-          dot += qv[d] * kp[p * D + d];
-          dd += gv[d] * vp[p * D + d];
-        }
-        sp[p] = pr->scale * dot;
-        da[p] = dd;
-      }
-      double mx = -INFINITY;
-      for (int64_t p = 0; p < P; ++p) mx = sp[p] > mx ? sp[p] : mx;
-      double l = 0.0;
-      for (int64_t p = 0; p < P; ++p) l += exp(sp[p] - mx);
-      double delta = 0.0;
-      for (int64_t p = 0; p < P; ++p) {
-        al[p] = exp(sp[p] - mx) / l;
-        delta += al[p] * da[p];
-      }
-      /* dq */
-      for (int64_t d = 0; d < D; ++d) {
-        double acc = 0.0;
-        for (int64_t p = 0; p < P; ++p) acc += al[p] * (da[p] - delta) * kp[p * D + d];
-        dq[n * D + d] = pr->scale * acc;
-      }
-      /* dK, dV scatter and offset gradients */
-      for (int64_t p = 0; p < P; ++p) {
-        const orc_point* s = &pts[p];
-        const double ds = al[p] * (da[p] - delta);
-        double g[3] = {0.0, 0.0, 0.0};
-        for (int c = 0; c < 8; ++c) {
-          if (!s->valid[c]) continue;
-          const int cx = c & 1, cy = (c >> 1) & 1, cz = (c >> 2) & 1;
-          const int64_t dst = ((s->crow[c] / pr->heads) % (pr->T * HW)) * D; /* (z,y,x) of batch b */
-          double qk = 0.0, dvv = 0.0;
-          for (int64_t d = 0; d < D; ++d) {
-            const double kc = ld(k, pr->bf16, s->crow[c] * D + d);
-            const double vc = ld(v, pr->bf16, s->crow[c] * D + d);
-            qk += qv[d] * kc;
-            dvv += gv[d] * vc;
-            const double addk = pr->scale * ds * s->w[c] * qv[d];
-            const double addv = al[p] * s->w[c] * gv[d];
-#pragma omp atomic
-            dk[dst + d] += addk;
-#pragma omp atomic
-            dv[dst + d] += addv;
-          }
-          const double G = pr->scale * ds * qk + al[p] * dvv;
-          const double ax[2] = {1.0 - s->frac[0], s->frac[0]};
-          const double ay[2] = {1.0 - s->frac[1], s->frac[1]};
-          const double az[2] = {1.0 - s->frac[2], s->frac[2]};
-          g[0] += G * (cx ? 1.0 : -1.0) * ay[cy] * az[cz];
-          g[1] += G * (cy ? 1.0 : -1.0) * ax[cx] * az[cz];
-          g[2] += G * (cz ? 1.0 : -1.0) * ax[cx] * ay[cy];
-        }
-        for (int a = 0; a < 3; ++a) doff[(n * P + p) * 3 + a] = g[a];
-      }
+      backward_query(pr, q, k, v, off, dout, b, t, i, j, m, dq + n * D, doff + n * P * 3, dk, dv, &w);
     }
-    free(pts);
-    free(kp);
-    free(vp);
-    free(qv);
-    free(gv);
-    free(sp);
-    free(al);
-    free(da);
+    scratch_free(&w);
+  }
+  return 0;
+}
+
+/*
+ * dq [nrows][D] and doff [nrows][P][3] of a list of query rows (flat (b, t, i, j, head)
+ * indices as in orc_forward).  No dK/dV: those gather contributions of many queries.
+ */
+int orc_backward_rows(const orc_problem* pr, const void* q, const void* k, const void* v,
+                      const float* off, const void* dout, const int64_t* rows, int64_t nrows,
+                      double* dq, double* doff) {
+  const int64_t P = pr->kt * pr->kh * pr->kw, D = pr->D;
+  if (P <= 0 || D <= 0) return -1;
+#pragma omp parallel
+  {
+    orc_scratch w;
+    scratch_alloc(&w, P, D);
+#pragma omp for schedule(dynamic, 4)
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int64_t row = rows[r];
+      const int64_t m = row % pr->heads, tok = row / pr->heads;
+      const int64_t j = tok % pr->W, i = (tok / pr->W) % pr->H, t = (tok / (pr->W * pr->H)) % pr->T;
+      const int64_t b = tok / (pr->W * pr->H * pr->T);
+      backward_query(pr, q, k, v, off, dout, b, t, i, j, m, dq + r * D, doff + r * P * 3, NULL, NULL,
+                     &w);
+    }
+    scratch_free(&w);
   }
   return 0;
 }

@@ -1,0 +1,11 @@
+"""3D Deformable Slide Attention (MegaSlide-DiT, Section 5.2, Eq. (1)) for MI355X (gfx950).
+
+The operator runs in the hand-written HIP kernels of ``libdsa3d.so`` behind the C ABI
+declared in ``include/dsa3d.h``.  This package holds the kernels (``csrc/``), the build
+script and a thin binding; PyTorch is used only for device memory and streams.
+"""
+from ._binding import (  # noqa: F401
+    DSA3D_BF16, DSA3D_F32, DSA3D_MAX_POINTS, DSA3D_OK, EXPORTED, Dsa3dError, dsa3d_abi_version,
+    dsa3d_backward, dsa3d_backward_workspace_size, dsa3d_desc, dsa3d_forward, load, make_desc,
+    status_string)
+from .ops import backward, forward  # noqa: F401

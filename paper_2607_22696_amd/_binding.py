@@ -1,0 +1,128 @@
+"""ctypes binding of libdsa3d.so with the same entry-point names as include/dsa3d.h.
+
+Argument marshalling only: descriptors are packed, tensors become device pointers and the
+current torch stream becomes the hipStream_t.  Every step of the operator runs in the HIP
+kernels of the library; there is no fallback, so a missing library is an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdsa3d.so")
+
+DSA3D_OK = 0
+DSA3D_ERR_NULL_POINTER = 1
+DSA3D_ERR_INVALID_SHAPE = 2
+DSA3D_ERR_UNSUPPORTED = 3
+DSA3D_ERR_MISALIGNED = 4
+DSA3D_ERR_WORKSPACE = 5
+DSA3D_ERR_ALIAS = 6
+DSA3D_ERR_DEVICE = 7
+
+DSA3D_F32 = 0
+DSA3D_BF16 = 1
+DSA3D_MAX_POINTS = 1024
+
+EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_workspace_size",
+            "dsa3d_status_string", "dsa3d_abi_version")
+
+
+class dsa3d_desc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("frames", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("kt", ctypes.c_int32), ("kh", ctypes.c_int32), ("kw", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class Dsa3dError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+_lib = None
+
+
+def load():
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_22696_amd/build.py "
+                              "(the operator has no non-HIP implementation)")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, pd = ctypes.c_void_p, ctypes.POINTER(dsa3d_desc)
+        lib.dsa3d_forward.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp]
+        lib.dsa3d_forward.restype = ctypes.c_int
+        lib.dsa3d_backward.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                       ctypes.c_size_t, vp]
+        lib.dsa3d_backward.restype = ctypes.c_int
+        lib.dsa3d_backward_workspace_size.argtypes = [pd]
+        lib.dsa3d_backward_workspace_size.restype = ctypes.c_size_t
+        lib.dsa3d_status_string.argtypes = [ctypes.c_int]
+        lib.dsa3d_status_string.restype = ctypes.c_char_p
+        lib.dsa3d_abi_version.argtypes = []
+        lib.dsa3d_abi_version.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def make_desc(B, T, H, W, heads, head_dim, kt, kh, kw, dtype="bf16", scale=0.0) -> dsa3d_desc:
+    return dsa3d_desc(B, T, H, W, heads, head_dim, kt, kh, kw, float(scale),
+                      DSA3D_BF16 if dtype == "bf16" else DSA3D_F32)
+
+
+def _ptr(x):
+    """Device pointer of a tensor (or an int address, or None for NULL)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def status_string(status: int) -> str:
+    return load().dsa3d_status_string(status).decode()
+
+
+def dsa3d_abi_version() -> int:
+    return load().dsa3d_abi_version()
+
+
+def dsa3d_backward_workspace_size(desc: dsa3d_desc) -> int:
+    return load().dsa3d_backward_workspace_size(ctypes.byref(desc))
+
+
+def dsa3d_forward(desc, q, k, v, offsets, out, lse=None, stream=None, check=True) -> int:
+    st = load().dsa3d_forward(ctypes.byref(desc) if desc is not None else None, _ptr(q), _ptr(k),
+                              _ptr(v), _ptr(offsets), _ptr(out), _ptr(lse), _stream(stream))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_forward")
+    return st
+
+
+def dsa3d_backward(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets,
+                   workspace=None, workspace_bytes=0, stream=None, check=True) -> int:
+    st = load().dsa3d_backward(ctypes.byref(desc) if desc is not None else None, _ptr(q), _ptr(k),
+                               _ptr(v), _ptr(offsets), _ptr(lse), _ptr(dout), _ptr(dq),
+                               _ptr(dk), _ptr(dv), _ptr(d_offsets), _ptr(workspace),
+                               workspace_bytes, _stream(stream))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_backward")
+    return st
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

@@ -1,0 +1,178 @@
+// C-ABI entry points of the 3D-DSA library: argument validation and kernel dispatch.
+// The operator and the conventions are described in include/dsa3d.h.
+#include "dsa3d.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "dsa3d_internal.h"
+
+namespace {
+
+struct Span {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+bool overlaps(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+Span span_of(const void* p, uint64_t bytes) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return Span{lo, lo + bytes};
+}
+
+// Checks the descriptor and fills the kernel geometry and the tensor sizes.
+dsa3d_status check_desc(const dsa3d_desc* d, dsa3d::Geometry* g, uint64_t* rows, uint64_t* io_bytes,
+                        uint64_t* f32_bytes, uint64_t* off_bytes) {
+  if (d == nullptr) return DSA3D_ERR_NULL_POINTER;
+  const int32_t dims[] = {d->batch, d->frames, d->height, d->width, d->heads, d->head_dim,
+                          d->kt, d->kh, d->kw};
+  for (int32_t x : dims)
+    if (x < 1) return DSA3D_ERR_INVALID_SHAPE;
+  if (d->kt % 2 == 0 || d->kh % 2 == 0 || d->kw % 2 == 0) return DSA3D_ERR_INVALID_SHAPE;
+  if (!std::isfinite(d->scale)) return DSA3D_ERR_INVALID_SHAPE;
+  // token coordinates must be exact in fp32
+  if (d->frames >= (1 << 24) || d->height >= (1 << 24) || d->width >= (1 << 24))
+    return DSA3D_ERR_INVALID_SHAPE;
+  const uint64_t N = (uint64_t)d->frames * d->height * d->width;
+  const uint64_t R = N * d->batch * d->heads;
+  if (N >= (1ull << 31) || R >= (1ull << 31)) return DSA3D_ERR_INVALID_SHAPE;
+  const uint64_t P = (uint64_t)d->kt * d->kh * d->kw;
+  if (d->dtype != DSA3D_F32 && d->dtype != DSA3D_BF16) return DSA3D_ERR_UNSUPPORTED;
+  if (d->head_dim != 32 && d->head_dim != 64 && d->head_dim != 128) return DSA3D_ERR_UNSUPPORTED;
+  if (P > DSA3D_MAX_POINTS) return DSA3D_ERR_UNSUPPORTED;
+  const uint64_t esz = d->dtype == DSA3D_BF16 ? 2 : 4;
+  g->B = d->batch;
+  g->T = d->frames;
+  g->H = d->height;
+  g->W = d->width;
+  g->heads = d->heads;
+  g->D = d->head_dim;
+  g->kt = d->kt;
+  g->kh = d->kh;
+  g->kw = d->kw;
+  g->P = (int)P;
+  g->N = (int)N;
+  g->scale = d->scale != 0.0f ? d->scale : 1.0f / std::sqrt((float)d->head_dim);
+  g->scale_log2 = g->scale * 1.4426950408889634f;
+  *rows = R;
+  *io_bytes = R * d->head_dim * esz;
+  *f32_bytes = R * d->head_dim * 4;
+  *off_bytes = R * P * 3 * 4;
+  return DSA3D_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dsa3d_abi_version(void) { return 1; }
+
+const char* dsa3d_status_string(dsa3d_status s) {
+  switch (s) {
+    case DSA3D_OK:
+      return "ok";
+    case DSA3D_ERR_NULL_POINTER:
+      return "a required pointer is NULL";
+    case DSA3D_ERR_INVALID_SHAPE:
+      return "invalid problem shape or scale";
+    case DSA3D_ERR_UNSUPPORTED:
+      return "unsupported dtype, head_dim or neighbourhood size";
+    case DSA3D_ERR_MISALIGNED:
+      return "misaligned pointer";
+    case DSA3D_ERR_WORKSPACE:
+      return "workspace too small";
+    case DSA3D_ERR_ALIAS:
+      return "an output overlaps another argument";
+    case DSA3D_ERR_DEVICE:
+      return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
+                           const float* offsets, void* out, float* lse, void* stream) {
+  dsa3d::Geometry g;
+  uint64_t rows, io_bytes, f32_bytes, off_bytes;
+  dsa3d_status st = check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes);
+  if (st != DSA3D_OK) return st;
+  if (!q || !k || !v || !offsets || !out) return DSA3D_ERR_NULL_POINTER;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(offsets, 4) || (lse && !aligned(lse, 4)))
+    return DSA3D_ERR_MISALIGNED;
+  const Span in[] = {span_of(q, io_bytes), span_of(k, io_bytes), span_of(v, io_bytes),
+                     span_of(offsets, off_bytes)};
+  const Span so = span_of(out, io_bytes);
+  for (const Span& s : in)
+    if (overlaps(so, s)) return DSA3D_ERR_ALIAS;
+  if (lse) {
+    const Span sl = span_of(lse, rows * 4);
+    if (overlaps(sl, so)) return DSA3D_ERR_ALIAS;
+    for (const Span& s : in)
+      if (overlaps(sl, s)) return DSA3D_ERR_ALIAS;
+  }
+  const hipError_t e = dsa3d::launch_forward(g, desc->dtype == DSA3D_BF16, q, k, v, offsets, out,
+                                             lse, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
+}
+
+// The backward bins every (query row, point) pair by its trilinear cell; bin ranks and entry
+// slots are 32-bit, so rows * P and the number of cells must stay below 2^31.
+static dsa3d_status check_backward_range(const dsa3d::Geometry& g, uint64_t rows) {
+  const uint64_t cells = (uint64_t)(g.T + 1) * (g.H + 1) * (g.W + 1) * g.B * g.heads;
+  if (rows * (uint64_t)g.P >= (1ull << 31) || cells >= (1ull << 31)) return DSA3D_ERR_INVALID_SHAPE;
+  return DSA3D_OK;
+}
+
+size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc) {
+  dsa3d::Geometry g;
+  uint64_t rows, io_bytes, f32_bytes, off_bytes;
+  if (check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes) != DSA3D_OK) return 0;
+  if (check_backward_range(g, rows) != DSA3D_OK) return 0;
+  return dsa3d::backward_workspace_bytes(g);
+}
+
+dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
+                            const float* offsets, const float* lse, const void* dout, float* dq,
+                            float* dk, float* dv, float* d_offsets, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  dsa3d::Geometry g;
+  uint64_t rows, io_bytes, f32_bytes, off_bytes;
+  dsa3d_status st = check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes);
+  if (st != DSA3D_OK) return st;
+  if (!q || !k || !v || !offsets || !lse || !dout || !dq || !dk || !dv || !d_offsets)
+    return DSA3D_ERR_NULL_POINTER;
+  st = check_backward_range(g, rows);
+  if (st != DSA3D_OK) return st;
+  const size_t ws_need = dsa3d::backward_workspace_bytes(g);
+  if (workspace == nullptr || workspace_bytes < ws_need) return DSA3D_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return DSA3D_ERR_MISALIGNED;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dout, 16) ||
+      !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) ||
+      !aligned(offsets, 4) || !aligned(lse, 4) || !aligned(d_offsets, 4))
+    return DSA3D_ERR_MISALIGNED;
+  const Span in[] = {span_of(q, io_bytes),         span_of(k, io_bytes),
+                     span_of(v, io_bytes),         span_of(offsets, off_bytes),
+                     span_of(lse, rows * 4),       span_of(dout, io_bytes)};
+  const Span outs[] = {span_of(dq, f32_bytes), span_of(dk, f32_bytes), span_of(dv, f32_bytes),
+                       span_of(d_offsets, off_bytes)};
+  const Span sw = span_of(workspace, ws_need);
+  for (int a = 0; a < 4; ++a) {
+    for (const Span& s : in)
+      if (overlaps(outs[a], s)) return DSA3D_ERR_ALIAS;
+    for (int b = a + 1; b < 4; ++b)
+      if (overlaps(outs[a], outs[b])) return DSA3D_ERR_ALIAS;
+    if (overlaps(outs[a], sw)) return DSA3D_ERR_ALIAS;
+  }
+  for (const Span& s : in)
+    if (overlaps(sw, s)) return DSA3D_ERR_ALIAS;
+  const hipError_t e = dsa3d::launch_backward(g, desc->dtype == DSA3D_BF16, q, k, v, offsets, lse,
+                                              dout, dq, dk, dv, d_offsets, workspace,
+                                              static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
+}
+
+}  // extern "C"

@@ -1,0 +1,509 @@
+// Backward of 3D Deformable Slide Attention (MegaSlide-DiT, Section 5.2, Eq. (1)).
+//
+// With alpha_p = softmax weights, da_p = <dout, v_p>, Delta = sum_p alpha_p da_p and
+// ds_p = alpha_p (da_p - Delta), the gradients are
+//   dq            = scale sum_p ds_p k_p
+//   d_offsets[p]  = sum_c dw_c/dpos (scale ds_p <q, K_c> + alpha_p <dout, V_c>)
+//   dK[x]         = sum over (query, point, corner c) landing on voxel x of scale ds_p w_c q
+//   dV[x]         = the same sum of alpha_p w_c dout
+//
+// Four launches, none with floating-point atomics:
+//  1. sweep (one L-lane group per query row, one pass over the points): loads the K and V
+//     corner rows, forms alpha_p and da_p, and keeps what depends on Delta factored:
+//       dq  = scale (sum_p alpha_p da_p k_p - Delta sum_p alpha_p k_p)
+//       d_offsets[p] = alpha_p (scale (da_p - Delta) A_p + B_p),
+//       A_p = sum_c dw_c/dpos <q, K_c>,  B_p = sum_c dw_c/dpos <dout, V_c>,
+//     so dq is final at the end of the sweep; A_p goes to d_offsets, (alpha_p, da_p, B_p)
+//     to a per-point record.  Every point is also counted into the bin of its trilinear
+//     cell (the floor of its position), and the returned count is its rank in the bin.
+//  2. exclusive scan of the bin counts -> bin starts.
+//  3. finalize (one thread per point): d_offsets from A_p, B_p and the row's Delta; the
+//     point's dK/dV coefficients (scale ds_p, alpha_p) and fractional position are written
+//     to slot start[cell] + rank, i.e. sorted by cell.
+//  4. gather (one L-lane group per voxel): a voxel is corner c of exactly the points whose
+//     cell is voxel - c, so it walks those 8 bins and accumulates w_c * coefficient * q and
+//     * dout rows in registers, then stores its dK and dV rows once.
+#include "dsa3d_device.h"
+
+namespace dsa3d {
+namespace {
+
+using namespace dev;
+
+// Per-point record of the sweep, read by the finalize pass.
+struct PointRec {
+  float alpha, dalpha, bx, by, bz;
+  int32_t rank;  // rank of the point in its cell's bin; -1 if no corner is inside the grid
+};
+
+// A point's contribution to dK/dV, stored in the bin of its cell.
+struct Entry {
+  int32_t n;      // query token within the batch item
+  float alpha;    // dV coefficient: alpha_p
+  float sds;      // dK coefficient: scale * ds_p
+  float fx, fy, fz;  // fractional position inside the cell
+};
+
+static_assert(sizeof(PointRec) == 24 && sizeof(Entry) == 24, "record layout");
+
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 16;
+constexpr int kScanBlockItems = kScanThreads * kScanItems;
+
+// Cells are the integer floor positions with at least one corner inside the grid:
+// x in [-1, W-1], y in [-1, H-1], z in [-1, T-1]; (T+1)(H+1)(W+1) of them per (b, head).
+__host__ __device__ inline int64_t cells_per_bh(const Geometry& g) {
+  return (int64_t)(g.T + 1) * (g.H + 1) * (g.W + 1);
+}
+
+__device__ inline int64_t cell_index(const Geometry& g, int bh, int x, int y, int z) {
+  return (int64_t)bh * cells_per_bh(g) + ((int64_t)(z + 1) * (g.H + 1) + (y + 1)) * (g.W + 1) + (x + 1);
+}
+
+__device__ inline bool cell_inside(const Geometry& g, int x, int y, int z) {
+  return x >= -1 && x < g.W && y >= -1 && y < g.H && z >= -1 && z < g.T;
+}
+
+// ---------------------------------------------------------------------------- 1. sweep
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
+    Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
+    const float* __restrict__ offsets, const float* __restrict__ lse,
+    const void* __restrict__ dout, float* __restrict__ dq, float* __restrict__ doff_a,
+    PointRec* __restrict__ recs, float* __restrict__ delta_out, uint32_t* __restrict__ counts,
+    int tiles) {
+  using LY = Layout<D, BF16>;
+  constexpr int L = LY::kLanes;
+  constexpr int VEC = LY::kVec;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / L, sub = lane % L;
+  const int64_t lane_off = (int64_t)sub * 16;
+  const char* qb = static_cast<const char*>(q);
+  const char* kb = static_cast<const char*>(k);
+  const char* vb = static_cast<const char*>(v);
+  const char* gb = static_cast<const char*>(dout);
+  const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+  const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
+
+  for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
+    const int bh = tile / tiles_per_bh;
+    const int b = bh / g.heads, m = bh % g.heads;
+    const int n = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
+    // All lanes of a group share n: a whole group is idle or active, so the group
+    // reductions never mix an idle group into an active one.
+    if (n >= g.N) continue;
+    const int j = n % g.W, i = (n / g.W) % g.H, t = n / (g.W * g.H);
+    const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
+
+    const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
+    const uint4 gr = load16(gb, row * LY::kRowBytes + lane_off);
+    const float lse2 = lse[row] * kLog2e;
+    const float* off = offsets + row * g.P * 3;
+    float ak[VEC], bk[VEC];
+#pragma unroll
+    for (int x = 0; x < VEC; ++x) {
+      ak[x] = 0.0f;
+      bk[x] = 0.0f;
+    }
+    float delta = 0.0f;
+
+    int it = 0, ih = 0, iw = 0;
+    for (int p = 0; p < g.P; ++p) {
+      Point pt;
+      make_point(g, b, t, i, j, m, it - rt, ih - rh, iw - rw, off + 3 * p, pt);
+      uint4 kr[8], vr[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        kr[c] = make_uint4(0, 0, 0, 0);
+        vr[c] = make_uint4(0, 0, 0, 0);
+        if (pt.ok[c]) {
+          kr[c] = load16(kb, pt.row[c] * LY::kRowBytes + lane_off);
+          vr[c] = load16(vb, pt.row[c] * LY::kRowBytes + lane_off);
+        }
+      }
+      float sp = 0.0f, dap = 0.0f;
+      float a3[3] = {0.0f, 0.0f, 0.0f}, b3[3] = {0.0f, 0.0f, 0.0f};
+      float kp[VEC];
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) kp[x] = 0.0f;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
+        const float qk = chunk_dot<BF16>(qr, kr[c]);
+        const float dvv = chunk_dot<BF16>(gr, vr[c]);
+        sp = fmaf(pt.w[c], qk, sp);
+        dap = fmaf(pt.w[c], dvv, dap);
+        // d w_c / d pos along each axis (corners outside the grid have zero rows)
+        const float wx = cx ? pt.ay[cy] * pt.az[cz] : -(pt.ay[cy] * pt.az[cz]);
+        const float wy = cy ? pt.ax[cx] * pt.az[cz] : -(pt.ax[cx] * pt.az[cz]);
+        const float wz = cz ? pt.ax[cx] * pt.ay[cy] : -(pt.ax[cx] * pt.ay[cy]);
+        a3[0] = fmaf(wx, qk, a3[0]);
+        a3[1] = fmaf(wy, qk, a3[1]);
+        a3[2] = fmaf(wz, qk, a3[2]);
+        b3[0] = fmaf(wx, dvv, b3[0]);
+        b3[1] = fmaf(wy, dvv, b3[1]);
+        b3[2] = fmaf(wz, dvv, b3[2]);
+        chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
+      }
+      const float alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
+      const float da = group_sum<L>(dap);
+      delta = fmaf(alpha, da, delta);
+      const float ada = alpha * da;
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) {
+        ak[x] = fmaf(ada, kp[x], ak[x]);
+        bk[x] = fmaf(alpha, kp[x], bk[x]);
+      }
+#pragma unroll
+      for (int a = 0; a < 3; ++a) {
+        a3[a] = group_sum<L>(a3[a]);
+        b3[a] = group_sum<L>(b3[a]);
+      }
+      if (sub == 0) {
+        const int64_t pidx = row * g.P + p;
+        doff_a[pidx * 3 + 0] = a3[0];
+        doff_a[pidx * 3 + 1] = a3[1];
+        doff_a[pidx * 3 + 2] = a3[2];
+        int32_t rank = -1;
+        if (cell_inside(g, pt.cx, pt.cy, pt.cz))
+          rank = (int32_t)atomicAdd(counts + cell_index(g, bh, pt.cx, pt.cy, pt.cz), 1u);
+        PointRec r;
+        r.alpha = alpha;
+        r.dalpha = da;
+        r.bx = b3[0];
+        r.by = b3[1];
+        r.bz = b3[2];
+        r.rank = rank;
+        recs[pidx] = r;
+      }
+      if (++iw == g.kw) {
+        iw = 0;
+        if (++ih == g.kh) {
+          ih = 0;
+          ++it;
+        }
+      }
+    }
+    float* dqr = dq + row * D + sub * VEC;
+#pragma unroll
+    for (int x = 0; x < VEC; x += 4)
+      *reinterpret_cast<float4*>(dqr + x) =
+          make_float4(g.scale * fmaf(-delta, bk[x], ak[x]), g.scale * fmaf(-delta, bk[x + 1], ak[x + 1]),
+                      g.scale * fmaf(-delta, bk[x + 2], ak[x + 2]),
+                      g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
+    if (sub == 0) delta_out[row] = delta;
+  }
+}
+
+// ---------------------------------------------------------------------------- 2. scan
+
+__global__ __launch_bounds__(kBlockThreads) void fill_u32_kernel(uint32_t* __restrict__ a, int64_t n,
+                                                                  uint32_t value) {
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
+       x += (int64_t)gridDim.x * blockDim.x)
+    a[x] = value;
+}
+
+// Exclusive scan of one 256-thread block's per-thread values; returns the block total.
+__device__ inline uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds_waves, uint32_t& excl) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t incl = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t o = __shfl_up(incl, d);
+    if (lane >= d) incl += o;
+  }
+  if (lane == 63) lds_waves[wave] = incl;
+  __syncthreads();
+  uint32_t wave_off = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kScanThreads / 64; ++w) {
+    const uint32_t s = lds_waves[w];
+    if (w < wave) wave_off += s;
+    total += s;
+  }
+  __syncthreads();
+  excl = wave_off + incl - v;
+  return total;
+}
+
+// Block sums of kScanBlockItems items each.
+__global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(const uint32_t* __restrict__ in,
+                                                                    uint32_t* __restrict__ sums,
+                                                                    int64_t n) {
+  __shared__ uint32_t lds[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanBlockItems + (int64_t)threadIdx.x * kScanItems;
+  uint32_t s = 0;
+#pragma unroll
+  for (int e = 0; e < kScanItems; ++e)
+    if (base + e < n) s += in[base + e];
+  uint32_t excl;
+  const uint32_t total = block_exclusive_scan(s, lds, excl);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+// Exclusive scan of the block sums in place (one block, chunk by chunk); writes the grand
+// total to *grand.
+__global__ __launch_bounds__(kScanThreads) void scan_sums_kernel(uint32_t* __restrict__ sums,
+                                                                  int64_t nsums,
+                                                                  uint32_t* __restrict__ grand) {
+  __shared__ uint32_t lds[kScanThreads / 64];
+  uint32_t carry = 0;
+  for (int64_t base = 0; base < nsums; base += kScanThreads) {
+    const int64_t x = base + threadIdx.x;
+    const uint32_t v = x < nsums ? sums[x] : 0u;
+    uint32_t excl;
+    const uint32_t total = block_exclusive_scan(v, lds, excl);
+    if (x < nsums) sums[x] = carry + excl;
+    carry += total;
+  }
+  if (threadIdx.x == 0) *grand = carry;
+}
+
+// starts[x] = offset of block + exclusive scan inside the block.
+__global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t* __restrict__ in,
+                                                                   const uint32_t* __restrict__ sums,
+                                                                   uint32_t* __restrict__ out,
+                                                                   int64_t n) {
+  __shared__ uint32_t lds[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanBlockItems + (int64_t)threadIdx.x * kScanItems;
+  uint32_t vals[kScanItems];
+  uint32_t s = 0;
+#pragma unroll
+  for (int e = 0; e < kScanItems; ++e) {
+    vals[e] = base + e < n ? in[base + e] : 0u;
+    s += vals[e];
+  }
+  uint32_t excl;
+  block_exclusive_scan(s, lds, excl);
+  uint32_t run = sums[blockIdx.x] + excl;
+#pragma unroll
+  for (int e = 0; e < kScanItems; ++e) {
+    if (base + e < n) out[base + e] = run;
+    run += vals[e];
+  }
+}
+
+// ---------------------------------------------------------------------------- 3. finalize
+
+__global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
+    Geometry g, const float* __restrict__ offsets, const PointRec* __restrict__ recs,
+    const float* __restrict__ delta, const uint32_t* __restrict__ starts, float* __restrict__ doff,
+    Entry* __restrict__ entries, int64_t npoints) {
+  const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < npoints;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = idx / g.P;
+    const int p = (int)(idx - row * g.P);
+    const PointRec r = recs[idx];
+    const float dd = r.dalpha - delta[row];
+    float* d = doff + idx * 3;
+    const float sa = g.scale * dd;
+    d[0] = r.alpha * fmaf(sa, d[0], r.bx);
+    d[1] = r.alpha * fmaf(sa, d[1], r.by);
+    d[2] = r.alpha * fmaf(sa, d[2], r.bz);
+    if (r.rank < 0) continue;
+    const int m = (int)(row % g.heads);
+    const int64_t tok = row / g.heads;
+    const int n = (int)(tok % g.N), b = (int)(tok / g.N);
+    const int j = n % g.W, i = (n / g.W) % g.H, t = n / (g.W * g.H);
+    const int iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
+    const float* o = offsets + idx * 3;
+    int x, y, z;
+    float fx, fy, fz;
+    axis((float)(j + iw - rw), o[0], g.W, x, fx);
+    axis((float)(i + ih - rh), o[1], g.H, y, fy);
+    axis((float)(t + it - rt), o[2], g.T, z, fz);
+    Entry e;
+    e.n = n;
+    e.alpha = r.alpha;
+    e.sds = g.scale * r.alpha * dd;
+    e.fx = fx;
+    e.fy = fy;
+    e.fz = fz;
+    entries[starts[cell_index(g, b * g.heads + m, x, y, z)] + (uint32_t)r.rank] = e;
+  }
+}
+
+// ---------------------------------------------------------------------------- 4. gather
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
+    Geometry g, const void* __restrict__ q, const void* __restrict__ dout,
+    const uint32_t* __restrict__ starts, const Entry* __restrict__ entries, float* __restrict__ dk,
+    float* __restrict__ dv, int tiles) {
+  using LY = Layout<D, BF16>;
+  constexpr int L = LY::kLanes;
+  constexpr int VEC = LY::kVec;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / L, sub = lane % L;
+  const int64_t lane_off = (int64_t)sub * 16;
+  const char* qb = static_cast<const char*>(q);
+  const char* gb = static_cast<const char*>(dout);
+  const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+
+  for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
+    const int bh = tile / tiles_per_bh;
+    const int b = bh / g.heads, m = bh % g.heads;
+    const int n = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
+    if (n >= g.N) continue;
+    const int x = n % g.W, y = (n / g.W) % g.H, z = n / (g.W * g.H);
+    const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
+    float ak[VEC], av[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      ak[e] = 0.0f;
+      av[e] = 0.0f;
+    }
+    // this voxel is corner c = (cx, cy, cz) of the points whose cell is voxel - c
+#pragma unroll 1
+    for (int c = 0; c < 8; ++c) {
+      const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
+      const int64_t ci = cell_index(g, bh, x - cx, y - cy, z - cz);
+      const uint32_t s = starts[ci], e_end = starts[ci + 1];
+      for (uint32_t u = s; u < e_end; ++u) {
+        const Entry en = entries[u];
+        const float w = (cx ? en.fx : 1.0f - en.fx) * (cy ? en.fy : 1.0f - en.fy) *
+                        (cz ? en.fz : 1.0f - en.fz);
+        const int64_t src = ((int64_t)b * g.N + en.n) * g.heads + m;
+        const uint4 qr = load16(qb, src * LY::kRowBytes + lane_off);
+        const uint4 gr = load16(gb, src * LY::kRowBytes + lane_off);
+        chunk_axpy<BF16>(ak, en.sds * w, qr);
+        chunk_axpy<BF16>(av, en.alpha * w, gr);
+      }
+    }
+    float* dkr = dk + row * D + sub * VEC;
+    float* dvr = dv + row * D + sub * VEC;
+#pragma unroll
+    for (int e = 0; e < VEC; e += 4) {
+      *reinterpret_cast<float4*>(dkr + e) = make_float4(ak[e], ak[e + 1], ak[e + 2], ak[e + 3]);
+      *reinterpret_cast<float4*>(dvr + e) = make_float4(av[e], av[e + 1], av[e + 2], av[e + 3]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------- launch
+
+struct Workspace {
+  uint32_t* counts;   // [cells]
+  uint32_t* starts;   // [cells + 1]
+  uint32_t* sums;     // [ceil(cells / kScanBlockItems)]
+  PointRec* recs;     // [rows * P]
+  float* delta;       // [rows]
+  Entry* entries;     // [rows * P]
+  size_t bytes;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+Workspace carve(const Geometry& g, void* base) {
+  const int64_t rows = (int64_t)g.B * g.N * g.heads;
+  const int64_t cells = cells_per_bh(g) * g.B * g.heads;
+  const int64_t nsums = (cells + kScanBlockItems - 1) / kScanBlockItems;
+  const int64_t points = rows * g.P;
+  Workspace w{};
+  size_t off = 0;
+  char* p = static_cast<char*>(base);
+  auto take = [&](size_t bytes) {
+    char* r = p ? p + off : nullptr;
+    off += align256(bytes);
+    return r;
+  };
+  w.counts = reinterpret_cast<uint32_t*>(take(cells * 4));
+  w.starts = reinterpret_cast<uint32_t*>(take((cells + 1) * 4));
+  w.sums = reinterpret_cast<uint32_t*>(take(nsums * 4));
+  w.recs = reinterpret_cast<PointRec*>(take(points * sizeof(PointRec)));
+  w.delta = reinterpret_cast<float*>(take(rows * 4));
+  w.entries = reinterpret_cast<Entry*>(take(points * sizeof(Entry)));
+  w.bytes = off;
+  return w;
+}
+
+int grid_for(int64_t items, int per_block = kBlockThreads, int cap = 1 << 20) {
+  const int64_t b = (items + per_block - 1) / per_block;
+  return (int)(b < 1 ? 1 : (b < cap ? b : cap));
+}
+
+template <int D, bool BF16>
+hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const void* v,
+                        const float* off, const float* lse, const void* dout, float* dq, float* dk,
+                        float* dv, float* doff, void* workspace, hipStream_t s) {
+  Workspace w = carve(g, workspace);
+  const int64_t rows = (int64_t)g.B * g.N * g.heads;
+  const int64_t cells = cells_per_bh(g) * g.B * g.heads;
+  const int64_t nsums = (cells + kScanBlockItems - 1) / kScanBlockItems;
+  const int64_t points = rows * g.P;
+  hipError_t e;
+  {
+    uint32_t zero = 0;
+    void* a[] = {(void*)&w.counts, (void*)&cells, (void*)&zero};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&fill_u32_kernel), dim3(grid_for(cells)),
+                        dim3(kBlockThreads), a, 0, s);
+    if (e != hipSuccess) return e;
+  }
+  const int tiles = tiles_for<D, BF16>(g);
+  const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
+  {
+    void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,      (void*)&v,       (void*)&off,
+                 (void*)&lse,  (void*)&dout,   (void*)&dq,     (void*)&doff,    (void*)&w.recs,
+                 (void*)&w.delta, (void*)&w.counts, (void*)&tiles};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16>), dim3(blocks),
+                        dim3(kBlockThreads), a, 0, s);
+    if (e != hipSuccess) return e;
+  }
+  {
+    void* a[] = {(void*)&w.counts, (void*)&w.sums, (void*)&cells};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_reduce_kernel), dim3((unsigned)nsums),
+                        dim3(kScanThreads), a, 0, s);
+    if (e != hipSuccess) return e;
+    uint32_t* grand = w.starts + cells;
+    void* b2[] = {(void*)&w.sums, (void*)&nsums, (void*)&grand};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_sums_kernel), dim3(1),
+                        dim3(kScanThreads), b2, 0, s);
+    if (e != hipSuccess) return e;
+    void* c3[] = {(void*)&w.counts, (void*)&w.sums, (void*)&w.starts, (void*)&cells};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_apply_kernel), dim3((unsigned)nsums),
+                        dim3(kScanThreads), c3, 0, s);
+    if (e != hipSuccess) return e;
+  }
+  {
+    void* a[] = {(void*)&g,        (void*)&off,   (void*)&w.recs, (void*)&w.delta,
+                 (void*)&w.starts, (void*)&doff,  (void*)&w.entries, (void*)&points};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_finalize_kernel), dim3(grid_for(points)),
+                        dim3(kBlockThreads), a, 0, s);
+    if (e != hipSuccess) return e;
+  }
+  {
+    void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
+                 (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&tiles};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16>), dim3(blocks),
+                        dim3(kBlockThreads), a, 0, s);
+  }
+  return e;
+}
+
+}  // namespace
+
+size_t backward_workspace_bytes(const Geometry& g) { return carve(g, nullptr).bytes; }
+
+hipError_t launch_backward(const Geometry& g, bool bf16, const void* q, const void* k,
+                           const void* v, const float* offsets, const float* lse, const void* dout,
+                           float* dq, float* dk, float* dv, float* d_offsets, void* workspace,
+                           hipStream_t stream) {
+#define DSA3D_BWD(DIM, BF) \
+  bwd_dispatch<DIM, BF>(g, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace, stream)
+  switch (g.D) {
+    case 32:
+      return bf16 ? DSA3D_BWD(32, true) : DSA3D_BWD(32, false);
+    case 64:
+      return bf16 ? DSA3D_BWD(64, true) : DSA3D_BWD(64, false);
+    case 128:
+      return bf16 ? DSA3D_BWD(128, true) : DSA3D_BWD(128, false);
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef DSA3D_BWD
+}
+
+}  // namespace dsa3d

@@ -1,0 +1,148 @@
+// Forward kernel of 3D Deformable Slide Attention (MegaSlide-DiT, Section 5.2, Eq. (1)).
+//
+// Each L-lane group owns one query row.  For every point it forms the sampling position,
+// the 8 trilinear corners and their weights in registers, loads the 8 K corner rows and
+// the 8 V corner rows (one 16-byte load per lane per row), reduces the interpolated logit
+// over the group with DPP butterflies (q.K by v_dot2_f32_bf16 on bf16 data, fp32
+// accumulation) and folds the point into an online (running-max, base-2) softmax, so each
+// corner row is read once.  Nothing per point is written to memory; the output row and
+// its LSE are stored once.
+//
+// Memory order: consecutive workgroups go to the 8 XCDs round-robin; blocks are renumbered
+// so each XCD walks one contiguous range of (batch, head, token) tiles and its L2 holds one
+// head's sliding band of K/V rows.
+#include "dsa3d_device.h"
+
+namespace dsa3d {
+namespace {
+
+using namespace dev;
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const void* __restrict__ q,
+                                                             const void* __restrict__ k,
+                                                             const void* __restrict__ v,
+                                                             const float* __restrict__ offsets,
+                                                             void* __restrict__ out,
+                                                             float* __restrict__ lse, int tiles) {
+  using LY = Layout<D, BF16>;
+  constexpr int L = LY::kLanes;
+  constexpr int VEC = LY::kVec;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / L, sub = lane % L;
+  const int64_t lane_off = (int64_t)sub * 16;
+  const char* qb = static_cast<const char*>(q);
+  const char* kb = static_cast<const char*>(k);
+  const char* vb = static_cast<const char*>(v);
+  const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+
+  for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
+    const int bh = tile / tiles_per_bh;
+    const int b = bh / g.heads, m = bh % g.heads;
+    const int n_raw = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
+    const bool active = n_raw < g.N;
+    const int n = active ? n_raw : g.N - 1;
+    const int j = n % g.W, i = (n / g.W) % g.H, t = n / (g.W * g.H);
+    const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
+
+    const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
+    const float* off = offsets + row * g.P * 3;
+    float o[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[e] = 0.0f;
+    float mx = -INFINITY, l = 0.0f;
+
+    int it = 0, ih = 0, iw = 0;
+    const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
+    for (int p = 0; p < g.P; ++p) {
+      Point pt;
+      make_point(g, b, t, i, j, m, it - rt, ih - rh, iw - rw, off + 3 * p, pt);
+      uint4 kr[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        kr[c] = make_uint4(0, 0, 0, 0);
+        if (pt.ok[c]) kr[c] = load16(kb, pt.row[c] * LY::kRowBytes + lane_off);
+      }
+      uint4 vr[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        vr[c] = make_uint4(0, 0, 0, 0);
+        if (pt.ok[c]) vr[c] = load16(vb, pt.row[c] * LY::kRowBytes + lane_off);
+      }
+      float sp = 0.0f;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) sp = fmaf(pt.w[c], chunk_dot<BF16>(qr, kr[c]), sp);
+      const float s2 = group_sum<L>(sp) * g.scale_log2;
+      // One exponential per point: a new maximum rescales the running sums by
+      // 2^(old max - new max) and enters with weight exactly 1; otherwise the point enters
+      // with 2^(s - max).  (The first point always takes the first branch: 2^-inf = 0.)
+      const bool up = s2 > mx;
+      const float ex = exp2f(up ? mx - s2 : s2 - mx);
+      const float corr = up ? ex : 1.0f;
+      const float e = up ? 1.0f : ex;
+      l = fmaf(l, corr, e);
+      mx = up ? s2 : mx;
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) o[x] *= corr;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) chunk_axpy<BF16>(o, e * pt.w[c], vr[c]);
+      if (++iw == g.kw) {
+        iw = 0;
+        if (++ih == g.kh) {
+          ih = 0;
+          ++it;
+        }
+      }
+    }
+    if (active) {
+      const float inv = 1.0f / l;
+      char* ob = static_cast<char*>(out) + row * LY::kRowBytes + lane_off;
+      if constexpr (BF16) {
+        uint4 w;
+        w.x = bf16_bits(o[0] * inv) | (bf16_bits(o[1] * inv) << 16);
+        w.y = bf16_bits(o[2] * inv) | (bf16_bits(o[3] * inv) << 16);
+        w.z = bf16_bits(o[4] * inv) | (bf16_bits(o[5] * inv) << 16);
+        w.w = bf16_bits(o[6] * inv) | (bf16_bits(o[7] * inv) << 16);
+        *reinterpret_cast<uint4*>(ob) = w;
+      } else {
+        *reinterpret_cast<float4*>(ob) = make_float4(o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
+      }
+      if (lse != nullptr && sub == 0) lse[row] = (mx + log2f(l)) * kLn2;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------- launch
+
+template <int D, bool BF16>
+hipError_t fwd_dispatch(const Geometry& g, const void* q, const void* k, const void* v,
+                        const float* off, void* out, float* lse, hipStream_t s) {
+  const int tiles = tiles_for<D, BF16>(g);
+  const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
+  void* args[] = {(void*)&g, (void*)&q, (void*)&k, (void*)&v, (void*)&off, (void*)&out, (void*)&lse,
+                  (void*)&tiles};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&fwd_kernel<D, BF16>), dim3(blocks),
+                         dim3(kBlockThreads), args, 0, s);
+}
+
+}  // namespace
+
+hipError_t launch_forward(const Geometry& g, bool bf16, const void* q, const void* k,
+                          const void* v, const float* offsets, void* out, float* lse,
+                          hipStream_t stream) {
+  switch (g.D) {
+    case 32:
+      return bf16 ? fwd_dispatch<32, true>(g, q, k, v, offsets, out, lse, stream)
+                  : fwd_dispatch<32, false>(g, q, k, v, offsets, out, lse, stream);
+    case 64:
+      return bf16 ? fwd_dispatch<64, true>(g, q, k, v, offsets, out, lse, stream)
+                  : fwd_dispatch<64, false>(g, q, k, v, offsets, out, lse, stream);
+    case 128:
+      return bf16 ? fwd_dispatch<128, true>(g, q, k, v, offsets, out, lse, stream)
+                  : fwd_dispatch<128, false>(g, q, k, v, offsets, out, lse, stream);
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace dsa3d

@@ -1,0 +1,165 @@
+"""CPU-side checks of the C ABI: the library loads, exports every declared entry point, and
+every validation error returns its status before anything is launched (all pointers here
+are fake host addresses; no call in this file reaches the GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_22696_amd as dsa
+from paper_2607_22696_amd import _binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "dsa3d.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dsa3d_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = ctypes.CDLL(B.LIB_PATH)
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTED), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_abi_version_and_status_strings():
+    assert dsa.dsa3d_abi_version() == 1
+    for s in range(0, 8):
+        assert isinstance(dsa.status_string(s), str) and dsa.status_string(s)
+    assert dsa.status_string(99) == "unknown status"
+
+
+def test_desc_layout_matches_header():
+    # 9 int32 dims + float scale + enum dtype
+    assert ctypes.sizeof(B.dsa3d_desc) == 11 * 4
+
+
+A = 1 << 20  # fake, well-aligned, non-overlapping "device" addresses (never dereferenced)
+
+
+def ptrs(n, stride=1 << 34, base=1 << 40):
+    return [base + i * stride for i in range(n)]
+
+
+def fwd(desc, **over):
+    q, k, v, off, out, lse = ptrs(6)
+    args = dict(q=q, k=k, v=v, offsets=off, out=out, lse=lse)
+    args.update(over)
+    return dsa.dsa3d_forward(desc, args["q"], args["k"], args["v"], args["offsets"], args["out"],
+                             args["lse"], stream=0, check=False)
+
+
+def bwd(desc, **over):
+    names = ["q", "k", "v", "offsets", "lse", "dout", "dq", "dk", "dv", "d_offsets", "workspace"]
+    args = dict(zip(names, ptrs(len(names))))
+    args["workspace_bytes"] = 1 << 33
+    args.update(over)
+    return dsa.dsa3d_backward(desc, *[args[n] for n in names[:-1]], workspace=args["workspace"],
+                              workspace_bytes=args["workspace_bytes"], stream=0, check=False)
+
+
+def good_desc(**kw):
+    d = dict(B=1, T=4, H=8, W=8, heads=2, head_dim=32, kt=3, kh=3, kw=3, dtype="f32", scale=0.0)
+    d.update(kw)
+    return dsa.make_desc(d["B"], d["T"], d["H"], d["W"], d["heads"], d["head_dim"], d["kt"],
+                         d["kh"], d["kw"], d["dtype"], d["scale"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(T=-1), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(heads=0), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(kt=2), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(kw=4), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(kh=0), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(scale=float("nan")), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(scale=float("inf")), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(T=1 << 16, H=1 << 16, W=2), B.DSA3D_ERR_INVALID_SHAPE),        # 2^33 tokens
+    (dict(T=1 << 12, H=1 << 10, W=1 << 8, heads=2), B.DSA3D_ERR_INVALID_SHAPE),  # 2^31 rows
+    (dict(head_dim=48), B.DSA3D_ERR_UNSUPPORTED),
+    (dict(head_dim=256), B.DSA3D_ERR_UNSUPPORTED),
+    (dict(kt=11, kh=11, kw=11), B.DSA3D_ERR_UNSUPPORTED),                 # P = 1331 > 1024
+])
+def test_descriptor_errors(kw, status):
+    d = good_desc(**kw)
+    assert fwd(d) == status
+    assert bwd(d) == status
+
+
+def test_bad_dtype():
+    d = good_desc()
+    d.dtype = 7
+    assert fwd(d) == B.DSA3D_ERR_UNSUPPORTED
+
+
+def test_null_pointers():
+    assert dsa.dsa3d_forward(None, *ptrs(6), stream=0, check=False) == B.DSA3D_ERR_NULL_POINTER
+    d = good_desc()
+    for name in ["q", "k", "v", "offsets", "out"]:
+        assert fwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+    for name in ["q", "k", "v", "offsets", "lse", "dout", "dq", "dk", "dv", "d_offsets"]:
+        assert bwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+
+
+def test_misaligned_pointers():
+    d = good_desc()
+    for name in ["q", "k", "v", "out"]:
+        p = ptrs(8)[7] + 8
+        assert fwd(d, **{name: p}) == B.DSA3D_ERR_MISALIGNED, name
+    assert fwd(d, offsets=ptrs(8)[7] + 2) == B.DSA3D_ERR_MISALIGNED
+    assert fwd(d, lse=ptrs(8)[7] + 1) == B.DSA3D_ERR_MISALIGNED
+    for name in ["q", "k", "v", "dout", "dq", "dk", "dv"]:
+        assert bwd(d, **{name: ptrs(16)[15] + 4}) == B.DSA3D_ERR_MISALIGNED, name
+    for name in ["offsets", "lse", "d_offsets"]:
+        assert bwd(d, **{name: ptrs(16)[15] + 2}) == B.DSA3D_ERR_MISALIGNED, name
+
+
+def test_overlapping_outputs():
+    d = good_desc()
+    q = ptrs(1)[0]
+    assert fwd(d, out=q) == B.DSA3D_ERR_ALIAS
+    assert fwd(d, out=q + 256) == B.DSA3D_ERR_ALIAS      # partial overlap of q's range
+    assert fwd(d, lse=q + 1024) == B.DSA3D_ERR_ALIAS
+    names = ptrs(10)
+    assert bwd(d, dk=names[6]) == B.DSA3D_ERR_ALIAS      # dk == dq
+    assert bwd(d, d_offsets=names[0] + 64) == B.DSA3D_ERR_ALIAS
+
+
+def test_workspace_size_follows_the_documented_formula():
+    for kw in (dict(), dict(B=2, T=5, H=7, W=9, heads=3, kt=3, kh=5, kw=5)):
+        d = good_desc(**kw)
+        rows = d.batch * d.frames * d.height * d.width * d.heads
+        P = d.kt * d.kh * d.kw
+        cells = d.batch * d.heads * (d.frames + 1) * (d.height + 1) * (d.width + 1)
+        ws = dsa.dsa3d_backward_workspace_size(d)
+        assert ws % 256 == 0
+        lo = 48 * rows * P + 8 * cells + 4 * rows
+        assert lo <= ws <= lo + 8 * 256 + 4 * (cells // 4096 + 1)
+    assert dsa.dsa3d_backward_workspace_size(good_desc(kt=2)) == 0
+
+
+def test_workspace_errors():
+    d = good_desc()
+    need = dsa.dsa3d_backward_workspace_size(d)
+    assert bwd(d, workspace=None) == B.DSA3D_ERR_WORKSPACE
+    assert bwd(d, workspace_bytes=need - 1) == B.DSA3D_ERR_WORKSPACE
+    assert bwd(d, workspace=ptrs(16)[15] + 128) == B.DSA3D_ERR_MISALIGNED
+    names = ptrs(11)
+    assert bwd(d, workspace=names[6]) == B.DSA3D_ERR_ALIAS          # workspace == dq
+    assert bwd(d, workspace=names[0], workspace_bytes=need) == B.DSA3D_ERR_ALIAS  # == q
+
+
+def test_backward_index_range_limit():
+    # 2^22 rows x 729 points > 2^31 (row, point) pairs: the forward accepts it, the
+    # backward's 32-bit bins do not.
+    d2 = good_desc(T=1 << 7, H=1 << 7, W=1 << 6, heads=2, kt=7, kh=7, kw=7)  # 2^21 rows, P=343
+    assert dsa.dsa3d_backward_workspace_size(d2) > 0  # 2^21 * 343 < 2^31
+    d3 = good_desc(T=1 << 8, H=1 << 7, W=1 << 6, heads=2, kt=9, kh=9, kw=9)  # 2^22 rows, P=729
+    assert dsa.dsa3d_backward_workspace_size(d3) == 0
+    assert bwd(d3) == B.DSA3D_ERR_INVALID_SHAPE
