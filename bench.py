@@ -51,25 +51,27 @@ def algorithmic(w):
     }
 
 
-def cpu_baseline(w, host, budget_s):
-    """The oracle (forward rows + backward slab with dK/dV scatter) on head 0, one frame at a
-    time, until about budget_s seconds of CPU work; reported in query tokens per second."""
+def cpu_baseline(w, host, budget_s, backward=True):
+    """The oracle (forward rows, plus the backward slab with its dK/dV scatter when the step
+    has a backward) on head 0, one frame at a time, until about budget_s seconds of CPU work;
+    reported in query tokens per second."""
     import numpy as np
 
     import oracle
     q, k, v, off, dout = host
     shape = (w.B, w.T, w.H, w.W, w.heads, w.head_dim, w.kt, w.kh, w.kw)
     HW = w.H * w.W
-    dk = np.zeros((w.T, w.H, w.W, w.head_dim))
-    dv = np.zeros_like(dk)
+    dk = np.zeros((w.T, w.H, w.W, w.head_dim)) if backward else None
+    dv = np.zeros_like(dk) if backward else None
     rows_done = 0
     frames = 0
     t0 = time.perf_counter()
     while frames < w.T and time.perf_counter() - t0 < budget_s:
         rows = (np.arange(HW, dtype=np.int64) + frames * HW) * w.heads  # head 0 of each token
         oracle.forward(shape, w.dtype, q, k, v, off, rows=rows)
-        oracle.backward_slab(shape, w.dtype, q, k, v, off, dout, 0, 0, frames, frames + 1,
-                             dk=dk, dv=dv)
+        if backward:
+            oracle.backward_slab(shape, w.dtype, q, k, v, off, dout, 0, 0, frames, frames + 1,
+                                 dk=dk, dv=dv)
         rows_done += HW
         frames += 1
     dt = time.perf_counter() - t0
@@ -77,7 +79,8 @@ def cpu_baseline(w, host, budget_s):
     return {"value": rows_done / w.heads / dt, "unit": "queries/s", "cores": oracle.threads(),
             "kind": "oracle",
             "sample": f"head 0 of frames [0,{frames}) of {w.name}: {rows_done} (token, head) rows, "
-                      f"forward + backward incl. dK/dV scatter, fp64, {dt:.1f} s; "
+                      + ("forward + backward incl. dK/dV scatter" if backward else "forward")
+                      + f", fp64, {dt:.1f} s; "
                       f"scaled to query tokens (all {w.heads} heads)"}
 
 
@@ -91,6 +94,9 @@ def main():
                     help="time the forward alone (workloads without a backward pass)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of CPU-oracle work for cpu_baseline (0 = skip)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run 3 device-to-device copies of MIB MiB and exit (calibrates the "
+                         "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -107,6 +113,21 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_probe:
+        n = args.copy_probe * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        t = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t[0].record()
+        for _ in range(3):
+            dst.copy_(src)
+        t[1].record()
+        torch.cuda.synchronize()
+        ms = t[0].elapsed_time(t[1]) / 3
+        print(json.dumps({"copy_mib": args.copy_probe, "ms": round(ms, 4),
+                          "gbs_read_plus_write": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}))
+        return
     dsa.load()
     w = testgen.WORKLOADS[args.workload]
     do_bwd = w.backward and not args.forward_only
@@ -201,7 +222,7 @@ def main():
         "input_gen_s": round(t_gen, 1),
     }
     if args.cpu_budget > 0:
-        res["cpu_baseline"] = cpu_baseline(w, host, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(w, host, args.cpu_budget, backward=do_bwd)
     print(json.dumps(res), flush=True)
 
 

@@ -58,6 +58,7 @@ dsa3d_status check_desc(const dsa3d_desc* d, dsa3d::Geometry* g, uint64_t* rows,
   g->N = (int)N;
   g->scale = d->scale != 0.0f ? d->scale : 1.0f / std::sqrt((float)d->head_dim);
   g->scale_log2 = g->scale * 1.4426950408889634f;
+  g->win_frames = dsa3d::window_frames(*g, (int)(d->head_dim * esz));
   *rows = R;
   *io_bytes = R * d->head_dim * esz;
   *f32_bytes = R * d->head_dim * 4;
@@ -66,6 +67,18 @@ dsa3d_status check_desc(const dsa3d_desc* d, dsa3d::Geometry* g, uint64_t* rows,
 }
 
 }  // namespace
+
+namespace dsa3d {
+
+int window_frames(const Geometry& g, int row_bytes) {
+  const uint64_t stride = (uint64_t)g.heads * row_bytes;
+  if (stride > 16383) return 0;  // the record stride field is 14 bits wide
+  const uint64_t frame_bytes = (uint64_t)g.H * g.W * stride;
+  const uint64_t frames = ((1ull << 32) - 4096) / frame_bytes;
+  return (int)(frames < (uint64_t)g.T ? frames : (uint64_t)g.T);
+}
+
+}  // namespace dsa3d
 
 extern "C" {
 

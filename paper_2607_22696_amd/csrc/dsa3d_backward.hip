@@ -78,28 +78,32 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
   constexpr int VEC = LY::kVec;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
-  const int64_t lane_off = (int64_t)sub * 16;
+  const int lane_off = sub * 16;
   const char* qb = static_cast<const char*>(q);
   const char* kb = static_cast<const char*>(k);
   const char* vb = static_cast<const char*>(v);
   const char* gb = static_cast<const char*>(dout);
   const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+  const int HW = g.H * g.W;
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
 
   for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int n = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
+    const int n0 = (tile % tiles_per_bh) * LY::kRowsPerBlock;
+    const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, n0 / HW);
+    const int n = n0 + wave * LY::kGroups + grp;
     // All lanes of a group share n: a whole group is idle or active, so the group
     // reductions never mix an idle group into an active one.
     if (n >= g.N) continue;
-    const int j = n % g.W, i = (n / g.W) % g.H, t = n / (g.W * g.H);
+    const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
     const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
     const uint4 gr = load16(gb, row * LY::kRowBytes + lane_off);
     const float lse2 = lse[row] * kLog2e;
     const float* off = offsets + row * g.P * 3;
+    float ox = off[0], oy = off[1], oz = off[2];
     float ak[VEC], bk[VEC];
 #pragma unroll
     for (int x = 0; x < VEC; ++x) {
@@ -111,17 +115,14 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
     int it = 0, ih = 0, iw = 0;
     for (int p = 0; p < g.P; ++p) {
       Point pt;
-      make_point(g, b, t, i, j, m, it - rt, ih - rh, iw - rw, off + 3 * p, pt);
-      uint4 kr[8], vr[8];
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        kr[c] = make_uint4(0, 0, 0, 0);
-        vr[c] = make_uint4(0, 0, 0, 0);
-        if (pt.ok[c]) {
-          kr[c] = load16(kb, pt.row[c] * LY::kRowBytes + lane_off);
-          vr[c] = load16(vb, pt.row[c] * LY::kRowBytes + lane_off);
-        }
+      make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, pt);
+      if (p + 1 < g.P) {  // next point's offsets, in flight with this point's corner rows
+        ox = off[3 * p + 3];
+        oy = off[3 * p + 4];
+        oz = off[3 * p + 5];
       }
+      uint4 kr[8], vr[8];
+      load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
       float sp = 0.0f, dap = 0.0f;
       float a3[3] = {0.0f, 0.0f, 0.0f}, b3[3] = {0.0f, 0.0f, 0.0f};
       float kp[VEC];
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
         const float dvv = chunk_dot<BF16>(gr, vr[c]);
         sp = fmaf(pt.w[c], qk, sp);
         dap = fmaf(pt.w[c], dvv, dap);
-        // d w_c / d pos along each axis (corners outside the grid have zero rows)
+        // d w_c / d pos along each axis (corners outside the grid have zero rows, so zero dots)
         const float wx = cx ? pt.ay[cy] * pt.az[cz] : -(pt.ay[cy] * pt.az[cz]);
         const float wy = cy ? pt.ax[cx] * pt.az[cz] : -(pt.ax[cx] * pt.az[cz]);
         const float wz = cz ? pt.ax[cx] * pt.ay[cy] : -(pt.ax[cx] * pt.ay[cy]);

@@ -126,19 +126,78 @@ __device__ inline __attribute__((always_inline)) int xcd_tile(int bid, int nbloc
   return xcd * per + min(xcd, rem) + slot;
 }
 
-// One sampling point of a query: corner rows, weights and validity (registers only).
+// ---------------------------------------------------------------------------- corner rows
+//
+// K and V rows are read through structured buffers: one record per token holds the rows of
+// all heads of that token (record stride = heads * row_bytes), the resource base sits at
+// head m of the first frame of a window of frames, and the record index of a voxel is
+// (z - t0) * H * W + y * W + x.  A corner outside the grid (or outside the window) gets an
+// index beyond the record count, and the buffer unit returns zeros for it: zero padding
+// without branches or masks.  A buffer covers at most 4 GB from its base, so for tensors
+// larger than that the window spans the frames around the block's own frame; the rare
+// corner inside the grid but outside the window is loaded by a plain global load.
+
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ i32x4_t dsa3d_struct_buffer_load_v4(__amdgpu_buffer_rsrc_t rsrc, int vindex, int voffset,
+                                              int soffset, int aux)
+    __asm("llvm.amdgcn.struct.ptr.buffer.load.v4i32");
+
+// Added to an index term to push a record index out of range.  Three of them stay below
+// 2^31, and every valid index is below 2^28 (a window spans < 4 GB of records >= 16 B).
+constexpr int kPoison = 1 << 29;
+// Third descriptor word for untyped 32-bit buffer access on gfx9-class GPUs.
+constexpr int kBufferFlags = 0x00020000;
+
+struct RowWindow {
+  __amdgpu_buffer_rsrc_t k, v;
+  int t0, frames;  // window [t0, t0 + frames); frames == 0: every corner takes the global path
+};
+
+// Window of batch item b, head m, centred on frame tc (all arguments wave-uniform).
+template <int ROW_BYTES>
+__device__ inline __attribute__((always_inline)) RowWindow make_window(const Geometry& g,
+                                                                       const void* k, const void* v,
+                                                                       int b, int m, int tc) {
+  RowWindow w;
+  w.frames = g.win_frames;
+  w.t0 = 0;
+  int64_t base = 0;
+  int nrec = 0;  // no window: zero records, so every buffer load returns zeros
+  short stride = 16;
+  if (w.frames > 0) {
+    w.t0 = min(max(tc - (w.frames - 1) / 2, 0), g.T - w.frames);
+    base = (((int64_t)b * g.T + w.t0) * g.H * g.W * g.heads + m) * ROW_BYTES;
+    nrec = w.frames * g.H * g.W;
+    stride = (short)(g.heads * ROW_BYTES);
+  }
+  w.k = __builtin_amdgcn_make_buffer_rsrc((void*)(static_cast<const char*>(k) + base), stride, nrec,
+                                          kBufferFlags);
+  w.v = __builtin_amdgcn_make_buffer_rsrc((void*)(static_cast<const char*>(v) + base), stride, nrec,
+                                          kBufferFlags);
+  return w;
+}
+
+__device__ inline __attribute__((always_inline)) uint4 buffer_row(__amdgpu_buffer_rsrc_t r, int vidx,
+                                                                  int lane_off) {
+  const i32x4_t x = dsa3d_struct_buffer_load_v4(r, vidx, lane_off, 0, 0);
+  return make_uint4((uint32_t)x.x, (uint32_t)x.y, (uint32_t)x.z, (uint32_t)x.w);
+}
+
+// One sampling point of a query: corner record indices and weights (registers only).
 struct Point {
-  int64_t row[8];  // row index of each corner in [B][T][H][W][heads]
-  float w[8];      // trilinear weight (0 for corners outside the grid)
-  bool ok[8];      // corner inside the grid
-  float ax[2], ay[2], az[2];  // per-axis weights (lower, upper corner), before zero padding
+  int vidx[8];                // record index of corner c = cz*4 + cy*2 + cx (out of range: zeros)
+  float w[8];                 // trilinear weight of corner c (corners outside read as zero rows)
+  float ax[2], ay[2], az[2];  // per-axis weights of the lower / upper corner
   int cx, cy, cz;             // floor of the (clamped) position: the trilinear cell
+  bool slow;                  // a corner inside the grid lies outside the buffer window
 };
 
 // pos = (float)(integer base) + offset, clamped to [-2, size + 1] (every corner of a position
 // beyond that range is outside the grid, so the clamp changes no value or gradient; it also
 // sends NaN to -2 and keeps the integer conversion in range).
-__device__ inline __attribute__((always_inline)) void axis(float base, float off, int size, int& i0, float& t) {
+__device__ inline __attribute__((always_inline)) void axis(float base, float off, int size, int& i0,
+                                                           float& t) {
   float p = base + off;
   p = fminf(fmaxf(p, -2.0f), (float)size + 1.0f);
   const float f = floorf(p);
@@ -146,13 +205,16 @@ __device__ inline __attribute__((always_inline)) void axis(float base, float off
   i0 = (int)f;
 }
 
-__device__ inline __attribute__((always_inline)) void make_point(const Geometry& g, int b, int t, int i, int j, int m,
-                                           int dz, int dy, int dx, const float* off, Point& pt) {
+__device__ inline __attribute__((always_inline)) void make_point(const Geometry& g,
+                                                                 const RowWindow& win, int t, int i,
+                                                                 int j, int dz, int dy, int dx,
+                                                                 float ox, float oy, float oz,
+                                                                 Point& pt) {
   int ix, iy, iz;
   float tx, ty, tz;
-  axis((float)(j + dx), off[0], g.W, ix, tx);
-  axis((float)(i + dy), off[1], g.H, iy, ty);
-  axis((float)(t + dz), off[2], g.T, iz, tz);
+  axis((float)(j + dx), ox, g.W, ix, tx);
+  axis((float)(i + dy), oy, g.H, iy, ty);
+  axis((float)(t + dz), oz, g.T, iz, tz);
   pt.ax[0] = 1.0f - tx;
   pt.ax[1] = tx;
   pt.ay[0] = 1.0f - ty;
@@ -162,17 +224,49 @@ __device__ inline __attribute__((always_inline)) void make_point(const Geometry&
   pt.cx = ix;
   pt.cy = iy;
   pt.cz = iz;
-  const bool vx[2] = {(unsigned)ix < (unsigned)g.W, (unsigned)(ix + 1) < (unsigned)g.W};
-  const bool vy[2] = {(unsigned)iy < (unsigned)g.H, (unsigned)(iy + 1) < (unsigned)g.H};
-  const bool vz[2] = {(unsigned)iz < (unsigned)g.T, (unsigned)(iz + 1) < (unsigned)g.T};
-  const int64_t sx = g.heads, sy = (int64_t)g.W * g.heads, sz = (int64_t)g.H * sy;
-  const int64_t r0 = ((((int64_t)b * g.T + iz) * g.H + iy) * g.W + ix) * g.heads + m;
+  const int HW = g.H * g.W;
+  const int zr = iz - win.t0;
+  const int xt[2] = {(unsigned)ix < (unsigned)g.W ? ix : kPoison,
+                     (unsigned)(ix + 1) < (unsigned)g.W ? ix + 1 : kPoison};
+  const int yt[2] = {(unsigned)iy < (unsigned)g.H ? iy * g.W : kPoison,
+                     (unsigned)(iy + 1) < (unsigned)g.H ? (iy + 1) * g.W : kPoison};
+  const int zt[2] = {(unsigned)zr < (unsigned)win.frames ? zr * HW : kPoison,
+                     (unsigned)(zr + 1) < (unsigned)win.frames ? (zr + 1) * HW : kPoison};
+  pt.slow = ((unsigned)iz < (unsigned)g.T && (unsigned)zr >= (unsigned)win.frames) ||
+            ((unsigned)(iz + 1) < (unsigned)g.T && (unsigned)(zr + 1) >= (unsigned)win.frames);
+  const float wyz[4] = {pt.ay[0] * pt.az[0], pt.ay[1] * pt.az[0], pt.ay[0] * pt.az[1],
+                        pt.ay[1] * pt.az[1]};
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
     const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
-    pt.ok[c] = vx[cx] && vy[cy] && vz[cz];
-    pt.w[c] = pt.ok[c] ? pt.ax[cx] * pt.ay[cy] * pt.az[cz] : 0.0f;
-    pt.row[c] = r0 + cx * sx + cy * sy + cz * sz;
+    pt.vidx[c] = xt[cx] + yt[cy] + zt[cz];
+    pt.w[c] = pt.ax[cx] * wyz[c >> 1];
+  }
+}
+
+// Loads the K and V rows (this lane's 16 bytes) of the 8 corners of a point.
+template <int ROW_BYTES>
+__device__ inline __attribute__((always_inline)) void load_corners(
+    const Geometry& g, const RowWindow& win, const char* kb, const char* vb, int b, int m,
+    int lane_off, const Point& pt, uint4* kr, uint4* vr) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    kr[c] = buffer_row(win.k, pt.vidx[c], lane_off);
+    vr[c] = buffer_row(win.v, pt.vidx[c], lane_off);
+  }
+  if (pt.slow) {
+    // corners inside the grid but outside the window: plain global loads
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int x = pt.cx + (c & 1), y = pt.cy + ((c >> 1) & 1), z = pt.cz + (c >> 2);
+      const bool inside = (unsigned)x < (unsigned)g.W && (unsigned)y < (unsigned)g.H &&
+                          (unsigned)z < (unsigned)g.T;
+      if (inside && (unsigned)(z - win.t0) >= (unsigned)win.frames) {
+        const int64_t row = ((((int64_t)b * g.T + z) * g.H + y) * g.W + x) * g.heads + m;
+        kr[c] = load16(kb, row * ROW_BYTES + lane_off);
+        vr[c] = load16(vb, row * ROW_BYTES + lane_off);
+      }
+    }
   }
 }
 

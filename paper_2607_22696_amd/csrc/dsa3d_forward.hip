@@ -2,7 +2,8 @@
 //
 // Each L-lane group owns one query row.  For every point it forms the sampling position,
 // the 8 trilinear corners and their weights in registers, loads the 8 K corner rows and
-// the 8 V corner rows (one 16-byte load per lane per row), reduces the interpolated logit
+// the 8 V corner rows (one 16-byte buffer load per lane per row; corners outside the grid
+// come back as zeros from the buffer unit), reduces the interpolated logit
 // over the group with DPP butterflies (q.K by v_dot2_f32_bf16 on bf16 data, fp32
 // accumulation) and folds the point into an online (running-max, base-2) softmax, so each
 // corner row is read once.  Nothing per point is written to memory; the output row and
@@ -30,19 +31,23 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const vo
   constexpr int VEC = LY::kVec;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
-  const int64_t lane_off = (int64_t)sub * 16;
+  const int lane_off = sub * 16;
   const char* qb = static_cast<const char*>(q);
   const char* kb = static_cast<const char*>(k);
   const char* vb = static_cast<const char*>(v);
   const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+  const int HW = g.H * g.W;
+  const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
 
   for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int n_raw = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
+    const int n0 = (tile % tiles_per_bh) * LY::kRowsPerBlock;
+    const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, n0 / HW);
+    const int n_raw = n0 + wave * LY::kGroups + grp;
     const bool active = n_raw < g.N;
     const int n = active ? n_raw : g.N - 1;
-    const int j = n % g.W, i = (n / g.W) % g.H, t = n / (g.W * g.H);
+    const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
     const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
@@ -51,24 +56,19 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const vo
 #pragma unroll
     for (int e = 0; e < VEC; ++e) o[e] = 0.0f;
     float mx = -INFINITY, l = 0.0f;
+    float ox = off[0], oy = off[1], oz = off[2];
 
     int it = 0, ih = 0, iw = 0;
-    const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
     for (int p = 0; p < g.P; ++p) {
       Point pt;
-      make_point(g, b, t, i, j, m, it - rt, ih - rh, iw - rw, off + 3 * p, pt);
-      uint4 kr[8];
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        kr[c] = make_uint4(0, 0, 0, 0);
-        if (pt.ok[c]) kr[c] = load16(kb, pt.row[c] * LY::kRowBytes + lane_off);
+      make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, pt);
+      if (p + 1 < g.P) {  // next point's offsets, in flight with this point's corner rows
+        ox = off[3 * p + 3];
+        oy = off[3 * p + 4];
+        oz = off[3 * p + 5];
       }
-      uint4 vr[8];
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        vr[c] = make_uint4(0, 0, 0, 0);
-        if (pt.ok[c]) vr[c] = load16(vb, pt.row[c] * LY::kRowBytes + lane_off);
-      }
+      uint4 kr[8], vr[8];
+      load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
       float sp = 0.0f;
 #pragma unroll
       for (int c = 0; c < 8; ++c) sp = fmaf(pt.w[c], chunk_dot<BF16>(qr, kr[c]), sp);

@@ -14,7 +14,12 @@ struct Geometry {
   int N;              // tokens per batch item, T*H*W
   float scale;        // logit scale (natural-log units)
   float scale_log2;   // scale * log2(e): logits are kept in base 2 inside the kernels
+  int win_frames;     // frames per K/V buffer window (0: corners are read with global loads)
 };
+
+// Frames of a K/V buffer window: a structured buffer addresses < 4 GB from its base and its
+// record stride (the rows of all heads of one token) must fit the descriptor's 14-bit field.
+int window_frames(const Geometry& g, int row_bytes);
 
 // All launches return the hipError_t of the launch itself.
 hipError_t launch_forward(const Geometry& g, bool bf16, const void* q, const void* k,

@@ -117,6 +117,10 @@ SMALL_CASES = [
     small("grid_1x1x1", T=1, H=1, W=1, heads=2, head_dim=32, seed=21),
     small("t1_bf16", T=1, H=9, W=17, heads=2, head_dim=64, dtype="bf16", seed=22),
     small("w1_f32", T=6, H=7, W=1, heads=2, head_dim=32, seed=23),
+    # 32 heads x 512-byte fp32 rows: a token's rows exceed the buffer record stride limit, so
+    # every corner takes the global-load path
+    small("wide_token_f32", T=2, H=4, W=5, heads=32, head_dim=128, seed=25,
+          offsets=testgen.Dist(testgen.UNIFORM, -2.0, 2.0)),
 ]
 
 
@@ -228,7 +232,7 @@ def full_size_backward(w, host, dev, out, lse, rows, slab_frames, slab_heads):
     sel = torch.from_numpy(rows).cuda()
     dq_h = to_host(dq.view(-1, D)[sel])
     doff_h = to_host(doff.view(-1, P * 3)[sel])
-    R = reach_frames(w, float(np.max(np.abs(off[..., 2]))))
+    R = reach_frames(w, float(np.max(np.abs(off[..., 2])))) if slab_frames else 0
     for m in slab_heads:
         for f in slab_frames:
             t0, t1 = max(0, f - R), min(T, f + 1 + R)
@@ -252,6 +256,20 @@ def test_full_scale_1080p_256f_forward_sampled():
     """2,088,960 tokens x 24 heads x 128, 3x3x3 kernel: the full grid runs on the GPU in the
     bench's launch configuration; 8192 sampled rows are checked."""
     full_size_forward(testgen.WORKLOADS["full_1080p_256f"], 8192)
+
+
+@pytest.mark.slow
+def test_window_fallback_large_temporal_offsets():
+    """K and V of 5 GB each: the buffer window covers 85 of the 100 frames, and offsets up to
+    +-60 tokens put many in-grid corners outside it, where the global-load path takes over."""
+    base = testgen.WORKLOADS["full_1080p_256f"]
+    w = base.with_grid(name="window_fallback", T=100, offsets=testgen.Dist(testgen.UNIFORM, -60.0, 60.0),
+                       seed=40, backward=True)
+    host, dev, out, lse, rows = full_size_forward(w, 4096)
+    q, k, v, off, dout = host
+    if dout is None:
+        dout = testgen.gen_tensor(w, testgen.TID_DOUT, w.qkv_shape(), w.dout, True)
+    full_size_backward(w, (q, k, v, off, dout), dev, out, lse, rows, slab_frames=[], slab_heads=[])
 
 
 @pytest.mark.slow
