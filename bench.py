@@ -28,6 +28,74 @@ METRIC = "3D-DSA fwd+bwd queries/s and achieved HBM GB/s (% of peak) at 1 GPU"
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 VALU_PEAK_TFLOPS = 157.3        # MI355X fp32 vector peak (2 FLOP/lane/clk: dot2 / dual issue)
 DEFAULT_WORKLOAD = "fwdbwd_64x34x60"
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2607_22696_amd", "csrc")
+
+
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources: counter figures taken from other sources are stale."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_family(name: str) -> str:
+    """Which entry point a kernel of the library belongs to."""
+    return "forward" if "fwd_kernel" in name else "backward"
+
+
+def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
+    """Turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE of the bench command, and of
+    a device copy of copy_mib MiB) into profiles/traffic_<workload>.json: HBM bytes per call of
+    each entry point, each counter scaled by what it reads for the copy of known size."""
+    import csv
+    import re
+
+    def per_kernel(d):
+        path = [os.path.join(d, f) for f in os.listdir(d) if f.endswith("counter_collection.csv")][0]
+        acc = {}
+        for r in csv.DictReader(open(path)):
+            m = re.search(r"(\w+_kernel)(<[^>]*>)?|(__amd_rocclr_copyBuffer)", r["Kernel_Name"])
+            key = m.group(0) if m else r["Kernel_Name"][:60]
+            acc.setdefault(key, []).append(float(r["Counter_Value"]) * 1024.0)  # KiB -> B
+        return acc
+
+    fetch, write = per_kernel(fetch_dir), per_kernel(write_dir)
+    true_bytes = copy_mib * (1 << 20)
+    cf = per_kernel(copyf_dir)["__amd_rocclr_copyBuffer"]
+    cw = per_kernel(copyw_dir)["__amd_rocclr_copyBuffer"]
+    fetch_scale = (sum(cf) / len(cf)) / true_bytes   # counter bytes per byte actually read
+    write_scale = (sum(cw) / len(cw)) / true_bytes
+    out = {"workload": workload, "kernel_source_hash": kernel_source_hash(),
+           "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
+           "kernels": {}, "per_call_bytes": {"forward": 0.0, "backward": 0.0}}
+    for k in fetch:
+        if k not in write or k == "__amd_rocclr_copyBuffer":
+            continue
+        f = sum(fetch[k]) / len(fetch[k]) / fetch_scale
+        w = sum(write[k]) / len(write[k]) / write_scale
+        out["kernels"][k] = {"fetch_bytes": round(f), "write_bytes": round(w)}
+        out["per_call_bytes"][kernel_family(k)] += f + w
+    os.makedirs(PROFILES, exist_ok=True)
+    path = os.path.join(PROFILES, f"traffic_{workload}.json")
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(path)
+
+
+def measured_traffic(workload, kernel_name):
+    """HBM bytes per call from profiles/traffic_<workload>.json, or None if absent or stale."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        d = json.load(fh)
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d["per_call_bytes"].get(kernel_name)
 
 
 def algorithmic(w):
@@ -94,11 +162,17 @@ def main():
                     help="time the forward alone (workloads without a backward pass)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of CPU-oracle work for cpu_baseline (0 = skip)")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH", "WRITE", "COPYF", "COPYW"),
+                    help="summarise four rocprofv3 --pmc output folders into "
+                         "profiles/traffic_<workload>.json (no GPU needed)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB and exit (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
     args = ap.parse_args()
 
+    if args.pmc_summary:
+        pmc_summary(args.workload, *args.pmc_summary, copy_mib=args.copy_probe or 1024)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the operator's "
               "multi-GPU sharding is a design note, not part of this build", file=sys.stderr)
@@ -194,7 +268,9 @@ def main():
         ach = kbytes / (kms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
-    roof["kernel"] = f"dsa3d {kname}"
+    tr = measured_traffic(w.name, kname)
+    roof["traffic"] = None if tr is None else round(tr)
+    roof["kernel"] = f"dsa3d_{kname}"
     roof["avg_launch_ms"] = round(kms, 4)
 
     res = {

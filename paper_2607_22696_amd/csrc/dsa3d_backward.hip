@@ -15,14 +15,15 @@
 //       A_p = sum_c dw_c/dpos <q, K_c>,  B_p = sum_c dw_c/dpos <dout, V_c>,
 //     so dq is final at the end of the sweep; A_p goes to d_offsets, (alpha_p, da_p, B_p)
 //     to a per-point record.  Every point is also counted into the bin of its trilinear
-//     cell (the floor of its position), and the returned count is its rank in the bin.
-//  2. exclusive scan of the bin counts -> bin starts.
+//     cell (the floor of its position) with an integer atomic whose result is not waited on.
+//  2. exclusive scan of the bin counts -> bin starts (and a copy used as fill cursors).
 //  3. finalize (one thread per point): d_offsets from A_p, B_p and the row's Delta; the
-//     point's dK/dV coefficients (scale ds_p, alpha_p) and fractional position are written
-//     to slot start[cell] + rank, i.e. sorted by cell.
+//     point claims a slot of its bin from the cursor and writes its dK/dV coefficients
+//     (scale ds_p, alpha_p) and fractional position there, i.e. sorted by cell.
 //  4. gather (one L-lane group per voxel): a voxel is corner c of exactly the points whose
-//     cell is voxel - c, so it walks those 8 bins and accumulates w_c * coefficient * q and
-//     * dout rows in registers, then stores its dK and dV rows once.
+//     cell is voxel - c, so it walks those 8 bins (4 contiguous ranges: cells x-1 and x are
+//     adjacent) and accumulates w_c * coefficient * q and * dout rows in registers, then
+//     stores its dK and dV rows once.
 #include "dsa3d_device.h"
 
 namespace dsa3d {
@@ -33,7 +34,6 @@ using namespace dev;
 // Per-point record of the sweep, read by the finalize pass.
 struct PointRec {
   float alpha, dalpha, bx, by, bz;
-  int32_t rank;  // rank of the point in its cell's bin; -1 if no corner is inside the grid
 };
 
 // A point's contribution to dK/dV, stored in the bin of its cell.
@@ -44,7 +44,7 @@ struct Entry {
   float fx, fy, fz;  // fractional position inside the cell
 };
 
-static_assert(sizeof(PointRec) == 24 && sizeof(Entry) == 24, "record layout");
+static_assert(sizeof(PointRec) == 20 && sizeof(Entry) == 24, "record layout");
 
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
@@ -166,16 +166,15 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
         doff_a[pidx * 3 + 0] = a3[0];
         doff_a[pidx * 3 + 1] = a3[1];
         doff_a[pidx * 3 + 2] = a3[2];
-        int32_t rank = -1;
-        if (cell_inside(g, pt.cx, pt.cy, pt.cz))
-          rank = (int32_t)atomicAdd(counts + cell_index(g, bh, pt.cx, pt.cy, pt.cz), 1u);
+        if (cell_inside(g, pt.cx, pt.cy, pt.cz))  // result unused: no wait on the atomic
+          __hip_atomic_fetch_add(counts + cell_index(g, bh, pt.cx, pt.cy, pt.cz), 1u,
+                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         PointRec r;
         r.alpha = alpha;
         r.dalpha = da;
         r.bx = b3[0];
         r.by = b3[1];
         r.bz = b3[2];
-        r.rank = rank;
         recs[pidx] = r;
       }
       if (++iw == g.kw) {
@@ -262,10 +261,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_sums_kernel(uint32_t* __res
   if (threadIdx.x == 0) *grand = carry;
 }
 
-// starts[x] = offset of block + exclusive scan inside the block.
+// starts[x] = cursor[x] = offset of block + exclusive scan inside the block.
 __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t* __restrict__ in,
                                                                    const uint32_t* __restrict__ sums,
                                                                    uint32_t* __restrict__ out,
+                                                                   uint32_t* __restrict__ cursor,
                                                                    int64_t n) {
   __shared__ uint32_t lds[kScanThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * kScanBlockItems + (int64_t)threadIdx.x * kScanItems;
@@ -281,7 +281,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t
   uint32_t run = sums[blockIdx.x] + excl;
 #pragma unroll
   for (int e = 0; e < kScanItems; ++e) {
-    if (base + e < n) out[base + e] = run;
+    if (base + e < n) {
+      out[base + e] = run;
+      cursor[base + e] = run;
+    }
     run += vals[e];
   }
 }
@@ -290,44 +293,52 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t
 
 __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
     Geometry g, const float* __restrict__ offsets, const PointRec* __restrict__ recs,
-    const float* __restrict__ delta, const uint32_t* __restrict__ starts, float* __restrict__ doff,
-    Entry* __restrict__ entries, int64_t npoints) {
+    const float* __restrict__ delta, uint32_t* __restrict__ cursor, float* __restrict__ doff,
+    Entry* __restrict__ entries, int npoints) {
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
-  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < npoints;
-       idx += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t row = idx / g.P;
-    const int p = (int)(idx - row * g.P);
+  const unsigned P = g.P, heads = g.heads, N = g.N, W = g.W, HW = g.H * g.W;
+  for (unsigned idx = blockIdx.x * blockDim.x + threadIdx.x; idx < (unsigned)npoints;
+       idx += gridDim.x * blockDim.x) {
+    const unsigned row = idx / P;
+    const unsigned p = idx - row * P;
     const PointRec r = recs[idx];
     const float dd = r.dalpha - delta[row];
-    float* d = doff + idx * 3;
+    float* d = doff + (size_t)idx * 3;
     const float sa = g.scale * dd;
     d[0] = r.alpha * fmaf(sa, d[0], r.bx);
     d[1] = r.alpha * fmaf(sa, d[1], r.by);
     d[2] = r.alpha * fmaf(sa, d[2], r.bz);
-    if (r.rank < 0) continue;
-    const int m = (int)(row % g.heads);
-    const int64_t tok = row / g.heads;
-    const int n = (int)(tok % g.N), b = (int)(tok / g.N);
-    const int j = n % g.W, i = (n / g.W) % g.H, t = n / (g.W * g.H);
-    const int iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
-    const float* o = offsets + idx * 3;
+    const unsigned tok = row / heads;
+    const unsigned m = row - tok * heads;
+    const unsigned b = tok / N;
+    const unsigned n = tok - b * N;
+    const unsigned t = n / HW;
+    const unsigned rem = n - t * HW;
+    const unsigned i = rem / W;
+    const unsigned j = rem - i * W;
+    const unsigned iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
+    const float* o = offsets + (size_t)idx * 3;
     int x, y, z;
     float fx, fy, fz;
-    axis((float)(j + iw - rw), o[0], g.W, x, fx);
-    axis((float)(i + ih - rh), o[1], g.H, y, fy);
-    axis((float)(t + it - rt), o[2], g.T, z, fz);
+    axis((float)((int)j + (int)iw - rw), o[0], g.W, x, fx);
+    axis((float)((int)i + (int)ih - rh), o[1], g.H, y, fy);
+    axis((float)((int)t + (int)it - rt), o[2], g.T, z, fz);
+    if (!cell_inside(g, x, y, z)) continue;
+    const uint32_t slot = atomicAdd(cursor + cell_index(g, b * heads + m, x, y, z), 1u);
     Entry e;
-    e.n = n;
+    e.n = (int32_t)n;
     e.alpha = r.alpha;
     e.sds = g.scale * r.alpha * dd;
     e.fx = fx;
     e.fy = fy;
     e.fz = fz;
-    entries[starts[cell_index(g, b * g.heads + m, x, y, z)] + (uint32_t)r.rank] = e;
+    entries[slot] = e;
   }
 }
 
 // ---------------------------------------------------------------------------- 4. gather
+
+constexpr int kGatherUnroll = 4;  // bin entries processed per iteration
 
 template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
@@ -337,18 +348,20 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
+  constexpr int U = kGatherUnroll;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
-  const int64_t lane_off = (int64_t)sub * 16;
-  const char* qb = static_cast<const char*>(q);
-  const char* gb = static_cast<const char*>(dout);
   const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+  const uint32_t tok_bytes = (uint32_t)g.heads * LY::kRowBytes;  // one token's rows, all heads
 
   for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
     const int n = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
     if (n >= g.N) continue;
+    const int64_t head_off = ((int64_t)b * g.N * g.heads + m) * LY::kRowBytes + sub * 16;
+    const char* qh = static_cast<const char*>(q) + head_off;
+    const char* gh = static_cast<const char*>(dout) + head_off;
     const int x = n % g.W, y = (n / g.W) % g.H, z = n / (g.W * g.H);
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
     float ak[VEC], av[VEC];
@@ -357,21 +370,33 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
       ak[e] = 0.0f;
       av[e] = 0.0f;
     }
-    // this voxel is corner c = (cx, cy, cz) of the points whose cell is voxel - c
+    // This voxel is corner (cx, cy, cz) of the points whose cell is voxel - (cx, cy, cz).
+    // For each (cy, cz), the bins of cells x-1 (corner cx = 1) and x (cx = 0) are adjacent.
 #pragma unroll 1
-    for (int c = 0; c < 8; ++c) {
-      const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
-      const int64_t ci = cell_index(g, bh, x - cx, y - cy, z - cz);
-      const uint32_t s = starts[ci], e_end = starts[ci + 1];
-      for (uint32_t u = s; u < e_end; ++u) {
-        const Entry en = entries[u];
-        const float w = (cx ? en.fx : 1.0f - en.fx) * (cy ? en.fy : 1.0f - en.fy) *
-                        (cz ? en.fz : 1.0f - en.fz);
-        const int64_t src = ((int64_t)b * g.N + en.n) * g.heads + m;
-        const uint4 qr = load16(qb, src * LY::kRowBytes + lane_off);
-        const uint4 gr = load16(gb, src * LY::kRowBytes + lane_off);
-        chunk_axpy<BF16>(ak, en.sds * w, qr);
-        chunk_axpy<BF16>(av, en.alpha * w, gr);
+    for (int r = 0; r < 4; ++r) {
+      const int cy = r & 1, cz = r >> 1;
+      const int64_t ci = cell_index(g, bh, x - 1, y - cy, z - cz);
+      const uint32_t s0 = starts[ci], mid = starts[ci + 1], end = starts[ci + 2];
+      for (uint32_t u = s0; u < end; u += U) {
+        Entry en[U];
+        uint4 qr[U], gr[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) en[k] = entries[min(u + k, end - 1)];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const uint64_t o = (uint64_t)(uint32_t)en[k].n * tok_bytes;
+          qr[k] = *reinterpret_cast<const uint4*>(qh + o);
+          gr[k] = *reinterpret_cast<const uint4*>(gh + o);
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const bool upper_x = (u + k) < mid;  // entry from cell x-1: this voxel is its cx = 1
+          float w = (upper_x ? en[k].fx : 1.0f - en[k].fx) * (cy ? en[k].fy : 1.0f - en[k].fy) *
+                    (cz ? en[k].fz : 1.0f - en[k].fz);
+          w = (u + k < end) ? w : 0.0f;
+          chunk_axpy<BF16>(ak, en[k].sds * w, qr[k]);
+          chunk_axpy<BF16>(av, en[k].alpha * w, gr[k]);
+        }
       }
     }
     float* dkr = dk + row * D + sub * VEC;
@@ -389,6 +414,7 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
 struct Workspace {
   uint32_t* counts;   // [cells]
   uint32_t* starts;   // [cells + 1]
+  uint32_t* cursor;   // [cells]
   uint32_t* sums;     // [ceil(cells / kScanBlockItems)]
   PointRec* recs;     // [rows * P]
   float* delta;       // [rows]
@@ -413,6 +439,7 @@ Workspace carve(const Geometry& g, void* base) {
   };
   w.counts = reinterpret_cast<uint32_t*>(take(cells * 4));
   w.starts = reinterpret_cast<uint32_t*>(take((cells + 1) * 4));
+  w.cursor = reinterpret_cast<uint32_t*>(take(cells * 4));
   w.sums = reinterpret_cast<uint32_t*>(take(nsums * 4));
   w.recs = reinterpret_cast<PointRec*>(take(points * sizeof(PointRec)));
   w.delta = reinterpret_cast<float*>(take(rows * 4));
@@ -463,14 +490,16 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_sums_kernel), dim3(1),
                         dim3(kScanThreads), b2, 0, s);
     if (e != hipSuccess) return e;
-    void* c3[] = {(void*)&w.counts, (void*)&w.sums, (void*)&w.starts, (void*)&cells};
+    void* c3[] = {(void*)&w.counts, (void*)&w.sums, (void*)&w.starts, (void*)&w.cursor,
+                  (void*)&cells};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_apply_kernel), dim3((unsigned)nsums),
                         dim3(kScanThreads), c3, 0, s);
     if (e != hipSuccess) return e;
   }
   {
+    const int npoints = (int)points;
     void* a[] = {(void*)&g,        (void*)&off,   (void*)&w.recs, (void*)&w.delta,
-                 (void*)&w.starts, (void*)&doff,  (void*)&w.entries, (void*)&points};
+                 (void*)&w.cursor, (void*)&doff,  (void*)&w.entries, (void*)&npoints};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_finalize_kernel), dim3(grid_for(points)),
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;

@@ -20,13 +20,15 @@ constexpr int kNumXcd = 8;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-template <int D, bool BF16>
+// NC = 16-byte chunks of a row per lane (1 or 2).
+template <int D, bool BF16, int NC = 1>
 struct Layout {
   static constexpr int kElemBytes = BF16 ? 2 : 4;
   static constexpr int kRowBytes = D * kElemBytes;
-  static constexpr int kLanes = kRowBytes / 16;  // lanes per query row
-  static constexpr int kVec = 16 / kElemBytes;   // channels per lane
-  static constexpr int kGroups = 64 / kLanes;    // query rows per wave
+  static constexpr int kChunks = NC;
+  static constexpr int kLanes = kRowBytes / (16 * NC);  // lanes per query row
+  static constexpr int kVec = 16 * NC / kElemBytes;      // channels per lane
+  static constexpr int kGroups = 64 / kLanes;            // query rows per wave
   static constexpr int kRowsPerBlock = kGroups * kWavesPerBlock;
   static_assert(kLanes >= 2 && kLanes <= 32, "unsupported head_dim");
 };
@@ -244,18 +246,19 @@ __device__ inline __attribute__((always_inline)) void make_point(const Geometry&
   }
 }
 
-// Loads the K and V rows (this lane's 16 bytes) of the 8 corners of a point.
-template <int ROW_BYTES>
-__device__ inline __attribute__((always_inline)) void load_corners(
-    const Geometry& g, const RowWindow& win, const char* kb, const char* vb, int b, int m,
-    int lane_off, const Point& pt, uint4* kr, uint4* vr) {
+// Loads one tensor's rows (this lane's NC x 16 bytes) at the 8 corners of a point through
+// the window resource `r`, with global loads from `base` for in-grid corners outside the
+// window; dst[c * NC + h] is chunk h of corner c.
+template <int ROW_BYTES, int NC = 1>
+__device__ inline __attribute__((always_inline)) void load_rows(
+    const Geometry& g, const RowWindow& win, __amdgpu_buffer_rsrc_t r, const char* base, int b,
+    int m, int lane_off, const Point& pt, uint4* dst) {
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
-    kr[c] = buffer_row(win.k, pt.vidx[c], lane_off);
-    vr[c] = buffer_row(win.v, pt.vidx[c], lane_off);
+#pragma unroll
+    for (int h = 0; h < NC; ++h) dst[c * NC + h] = buffer_row(r, pt.vidx[c], lane_off + 16 * h);
   }
   if (pt.slow) {
-    // corners inside the grid but outside the window: plain global loads
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       const int x = pt.cx + (c & 1), y = pt.cy + ((c >> 1) & 1), z = pt.cz + (c >> 2);
@@ -263,20 +266,30 @@ __device__ inline __attribute__((always_inline)) void load_corners(
                           (unsigned)z < (unsigned)g.T;
       if (inside && (unsigned)(z - win.t0) >= (unsigned)win.frames) {
         const int64_t row = ((((int64_t)b * g.T + z) * g.H + y) * g.W + x) * g.heads + m;
-        kr[c] = load16(kb, row * ROW_BYTES + lane_off);
-        vr[c] = load16(vb, row * ROW_BYTES + lane_off);
+#pragma unroll
+        for (int h = 0; h < NC; ++h)
+          dst[c * NC + h] = load16(base, row * ROW_BYTES + lane_off + 16 * h);
       }
     }
   }
+}
+
+// K and V rows of the 8 corners of a point.
+template <int ROW_BYTES, int NC = 1>
+__device__ inline __attribute__((always_inline)) void load_corners(
+    const Geometry& g, const RowWindow& win, const char* kb, const char* vb, int b, int m,
+    int lane_off, const Point& pt, uint4* kr, uint4* vr) {
+  load_rows<ROW_BYTES, NC>(g, win, win.k, kb, b, m, lane_off, pt, kr);
+  load_rows<ROW_BYTES, NC>(g, win, win.v, vb, b, m, lane_off, pt, vr);
 }
 
 // ---------------------------------------------------------------------------- launch shape
 
 constexpr int kMaxBlocks = 1 << 22;  // grid cap; larger problems loop over tiles
 
-template <int D, bool BF16>
+template <int D, bool BF16, int NC = 1>
 inline int tiles_for(const Geometry& g) {
-  using LY = Layout<D, BF16>;
+  using LY = Layout<D, BF16, NC>;
   const int64_t per = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   return (int)(per * g.B * g.heads);
 }

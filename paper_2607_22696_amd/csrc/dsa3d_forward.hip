@@ -19,19 +19,20 @@ namespace {
 
 using namespace dev;
 
-template <int D, bool BF16>
+template <int D, bool BF16, int NC>
 __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const void* __restrict__ q,
                                                              const void* __restrict__ k,
                                                              const void* __restrict__ v,
                                                              const float* __restrict__ offsets,
                                                              void* __restrict__ out,
                                                              float* __restrict__ lse, int tiles) {
-  using LY = Layout<D, BF16>;
+  using LY = Layout<D, BF16, NC>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
+  constexpr int CV = VEC / NC;  // channels per 16-byte chunk
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
-  const int lane_off = sub * 16;
+  const int lane_off = sub * 16 * NC;
   const char* qb = static_cast<const char*>(q);
   const char* kb = static_cast<const char*>(k);
   const char* vb = static_cast<const char*>(v);
@@ -50,7 +51,9 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const vo
     const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
-    const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
+    uint4 qr[NC];
+#pragma unroll
+    for (int h = 0; h < NC; ++h) qr[h] = load16(qb, row * LY::kRowBytes + lane_off + 16 * h);
     const float* off = offsets + row * g.P * 3;
     float o[VEC];
 #pragma unroll
@@ -67,11 +70,16 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const vo
         oy = off[3 * p + 4];
         oz = off[3 * p + 5];
       }
-      uint4 kr[8], vr[8];
-      load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
+      uint4 kr[8 * NC], vr[8 * NC];
+      load_corners<LY::kRowBytes, NC>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
       float sp = 0.0f;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) sp = fmaf(pt.w[c], chunk_dot<BF16>(qr, kr[c]), sp);
+      for (int c = 0; c < 8; ++c) {
+        float d = chunk_dot<BF16>(qr[0], kr[c * NC]);
+#pragma unroll
+        for (int h = 1; h < NC; ++h) d += chunk_dot<BF16>(qr[h], kr[c * NC + h]);
+        sp = fmaf(pt.w[c], d, sp);
+      }
       const float s2 = group_sum<L>(sp) * g.scale_log2;
       // One exponential per point: a new maximum rescales the running sums by
       // 2^(old max - new max) and enters with weight exactly 1; otherwise the point enters
@@ -85,7 +93,10 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const vo
 #pragma unroll
       for (int x = 0; x < VEC; ++x) o[x] *= corr;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) chunk_axpy<BF16>(o, e * pt.w[c], vr[c]);
+      for (int c = 0; c < 8; ++c) {
+#pragma unroll
+        for (int h = 0; h < NC; ++h) chunk_axpy<BF16>(o + h * CV, e * pt.w[c], vr[c * NC + h]);
+      }
       if (++iw == g.kw) {
         iw = 0;
         if (++ih == g.kh) {
@@ -97,15 +108,20 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const vo
     if (active) {
       const float inv = 1.0f / l;
       char* ob = static_cast<char*>(out) + row * LY::kRowBytes + lane_off;
-      if constexpr (BF16) {
-        uint4 w;
-        w.x = bf16_bits(o[0] * inv) | (bf16_bits(o[1] * inv) << 16);
-        w.y = bf16_bits(o[2] * inv) | (bf16_bits(o[3] * inv) << 16);
-        w.z = bf16_bits(o[4] * inv) | (bf16_bits(o[5] * inv) << 16);
-        w.w = bf16_bits(o[6] * inv) | (bf16_bits(o[7] * inv) << 16);
-        *reinterpret_cast<uint4*>(ob) = w;
-      } else {
-        *reinterpret_cast<float4*>(ob) = make_float4(o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
+#pragma unroll
+      for (int h = 0; h < NC; ++h) {
+        const float* oh = o + h * CV;
+        if constexpr (BF16) {
+          uint4 w;
+          w.x = bf16_bits(oh[0] * inv) | (bf16_bits(oh[1] * inv) << 16);
+          w.y = bf16_bits(oh[2] * inv) | (bf16_bits(oh[3] * inv) << 16);
+          w.z = bf16_bits(oh[4] * inv) | (bf16_bits(oh[5] * inv) << 16);
+          w.w = bf16_bits(oh[6] * inv) | (bf16_bits(oh[7] * inv) << 16);
+          *reinterpret_cast<uint4*>(ob + 16 * h) = w;
+        } else {
+          *reinterpret_cast<float4*>(ob + 16 * h) =
+              make_float4(oh[0] * inv, oh[1] * inv, oh[2] * inv, oh[3] * inv);
+        }
       }
       if (lse != nullptr && sub == 0) lse[row] = (mx + log2f(l)) * kLn2;
     }
@@ -114,14 +130,14 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(Geometry g, const vo
 
 // ---------------------------------------------------------------------------- launch
 
-template <int D, bool BF16>
+template <int D, bool BF16, int NC>
 hipError_t fwd_dispatch(const Geometry& g, const void* q, const void* k, const void* v,
                         const float* off, void* out, float* lse, hipStream_t s) {
-  const int tiles = tiles_for<D, BF16>(g);
+  const int tiles = tiles_for<D, BF16, NC>(g);
   const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
   void* args[] = {(void*)&g, (void*)&q, (void*)&k, (void*)&v, (void*)&off, (void*)&out, (void*)&lse,
                   (void*)&tiles};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&fwd_kernel<D, BF16>), dim3(blocks),
+  return hipLaunchKernel(reinterpret_cast<const void*>(&fwd_kernel<D, BF16, NC>), dim3(blocks),
                          dim3(kBlockThreads), args, 0, s);
 }
 
@@ -132,14 +148,14 @@ hipError_t launch_forward(const Geometry& g, bool bf16, const void* q, const voi
                           hipStream_t stream) {
   switch (g.D) {
     case 32:
-      return bf16 ? fwd_dispatch<32, true>(g, q, k, v, offsets, out, lse, stream)
-                  : fwd_dispatch<32, false>(g, q, k, v, offsets, out, lse, stream);
+      return bf16 ? fwd_dispatch<32, true, 1>(g, q, k, v, offsets, out, lse, stream)
+                  : fwd_dispatch<32, false, 1>(g, q, k, v, offsets, out, lse, stream);
     case 64:
-      return bf16 ? fwd_dispatch<64, true>(g, q, k, v, offsets, out, lse, stream)
-                  : fwd_dispatch<64, false>(g, q, k, v, offsets, out, lse, stream);
+      return bf16 ? fwd_dispatch<64, true, 1>(g, q, k, v, offsets, out, lse, stream)
+                  : fwd_dispatch<64, false, 1>(g, q, k, v, offsets, out, lse, stream);
     case 128:
-      return bf16 ? fwd_dispatch<128, true>(g, q, k, v, offsets, out, lse, stream)
-                  : fwd_dispatch<128, false>(g, q, k, v, offsets, out, lse, stream);
+      return bf16 ? fwd_dispatch<128, true, 1>(g, q, k, v, offsets, out, lse, stream)
+                  : fwd_dispatch<128, false, 1>(g, q, k, v, offsets, out, lse, stream);
     default:
       return hipErrorInvalidValue;
   }
