@@ -13,17 +13,20 @@
 //       dq  = scale (sum_p alpha_p da_p k_p - Delta sum_p alpha_p k_p)
 //       d_offsets[p] = alpha_p (scale (da_p - Delta) A_p + B_p),
 //       A_p = sum_c dw_c/dpos <q, K_c>,  B_p = sum_c dw_c/dpos <dout, V_c>,
-//     so dq is final at the end of the sweep; A_p goes to d_offsets, (alpha_p, da_p, B_p)
-//     to a per-point record.  Every point is also counted into the bin of its trilinear
-//     cell (the floor of its position) with an integer atomic whose result is not waited on.
+//     so dq is final at the end of the sweep; (alpha_p, da_p, A_p, B_p) go to a 32-byte
+//     record per point (lane k of a row keeps point k of each chunk of L points, and the
+//     row stores the chunk's records as one contiguous block).  Every point is also counted
+//     into the bin of its trilinear cell (the floor of its position) with an integer atomic
+//     whose result is not waited on.
 //  2. exclusive scan of the bin counts -> bin starts (and a copy used as fill cursors).
 //  3. finalize (one thread per point): d_offsets from A_p, B_p and the row's Delta; the
 //     point claims a slot of its bin from the cursor and writes its dK/dV coefficients
 //     (scale ds_p, alpha_p) and fractional position there, i.e. sorted by cell.
-//  4. gather (one L-lane group per voxel): a voxel is corner c of exactly the points whose
-//     cell is voxel - c, so it walks those 8 bins (4 contiguous ranges: cells x-1 and x are
-//     adjacent) and accumulates w_c * coefficient * q and * dout rows in registers, then
-//     stores its dK and dV rows once.
+//  4. gather (one L-lane group per pair of voxels adjacent along x): a voxel is corner c of
+//     exactly the points whose cell is voxel - c; for the pair these bins form 4 contiguous
+//     runs (cells x0-1, x0, x0+1 are adjacent), and the group accumulates
+//     w_c * coefficient * q and * dout rows in registers, then stores the dK and dV rows of
+//     both voxels once.
 #include "dsa3d_device.h"
 
 namespace dsa3d {
@@ -32,8 +35,8 @@ namespace {
 using namespace dev;
 
 // Per-point record of the sweep, read by the finalize pass.
-struct PointRec {
-  float alpha, dalpha, bx, by, bz;
+struct __align__(16) PointRec {
+  float alpha, dalpha, ax, ay, az, bx, by, bz;
 };
 
 // A point's contribution to dK/dV, stored in the bin of its cell.
@@ -44,7 +47,7 @@ struct Entry {
   float fx, fy, fz;  // fractional position inside the cell
 };
 
-static_assert(sizeof(PointRec) == 20 && sizeof(Entry) == 24, "record layout");
+static_assert(sizeof(PointRec) == 32 && sizeof(Entry) == 24, "record layout");
 
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
@@ -70,9 +73,8 @@ template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
     const float* __restrict__ offsets, const float* __restrict__ lse,
-    const void* __restrict__ dout, float* __restrict__ dq, float* __restrict__ doff_a,
-    PointRec* __restrict__ recs, float* __restrict__ delta_out, uint32_t* __restrict__ counts,
-    int tiles) {
+    const void* __restrict__ dout, float* __restrict__ dq, PointRec* __restrict__ recs,
+    float* __restrict__ delta_out, uint32_t* __restrict__ counts, int tiles) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -111,6 +113,7 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
       bk[x] = 0.0f;
     }
     float delta = 0.0f;
+    float4 rec[2];
 
     int it = 0, ih = 0, iw = 0;
     for (int p = 0; p < g.P; ++p) {
@@ -161,21 +164,20 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
         a3[a] = group_sum<L>(a3[a]);
         b3[a] = group_sum<L>(b3[a]);
       }
-      if (sub == 0) {
-        const int64_t pidx = row * g.P + p;
-        doff_a[pidx * 3 + 0] = a3[0];
-        doff_a[pidx * 3 + 1] = a3[1];
-        doff_a[pidx * 3 + 2] = a3[2];
-        if (cell_inside(g, pt.cx, pt.cy, pt.cz))  // result unused: no wait on the atomic
-          __hip_atomic_fetch_add(counts + cell_index(g, bh, pt.cx, pt.cy, pt.cz), 1u,
-                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        PointRec r;
-        r.alpha = alpha;
-        r.dalpha = da;
-        r.bx = b3[0];
-        r.by = b3[1];
-        r.bz = b3[2];
-        recs[pidx] = r;
+      if (sub == 0 && cell_inside(g, pt.cx, pt.cy, pt.cz))  // result unused: no wait
+        __hip_atomic_fetch_add(counts + cell_index(g, bh, pt.cx, pt.cy, pt.cz), 1u,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // lane (p mod L) of the row keeps this point's record; one store per chunk of L points
+      if (sub == p % L) {
+        rec[0] = make_float4(alpha, da, a3[0], a3[1]);
+        rec[1] = make_float4(a3[2], b3[0], b3[1], b3[2]);
+      }
+      if (p % L == L - 1 || p == g.P - 1) {
+        if (sub <= p % L) {
+          float4* dst = reinterpret_cast<float4*>(recs + row * g.P + (p - p % L) + sub);
+          dst[0] = rec[0];
+          dst[1] = rec[1];
+        }
       }
       if (++iw == g.kw) {
         iw = 0;
@@ -305,9 +307,9 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
     const float dd = r.dalpha - delta[row];
     float* d = doff + (size_t)idx * 3;
     const float sa = g.scale * dd;
-    d[0] = r.alpha * fmaf(sa, d[0], r.bx);
-    d[1] = r.alpha * fmaf(sa, d[1], r.by);
-    d[2] = r.alpha * fmaf(sa, d[2], r.bz);
+    d[0] = r.alpha * fmaf(sa, r.ax, r.bx);
+    d[1] = r.alpha * fmaf(sa, r.ay, r.by);
+    d[2] = r.alpha * fmaf(sa, r.az, r.bz);
     const unsigned tok = row / heads;
     const unsigned m = row - tok * heads;
     const unsigned b = tok / N;
@@ -340,6 +342,12 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
 
 constexpr int kGatherUnroll = 4;  // bin entries processed per iteration
 
+// Each L-lane group owns two voxels adjacent along x, (x0, x0 + 1).  For a (cy, cz) corner
+// pair, the voxels are corners of the points in cells x0-1 (x0 only, as cx = 1), x0 (both:
+// cx = 0 for x0, cx = 1 for x0 + 1) and x0+1 (x0 + 1 only, as cx = 0); those three bins are
+// adjacent, so one contiguous run of entries serves both voxels and every entry's q and dout
+// rows are loaded once for the pair.  Entries are read one batch ahead, so a batch waits for
+// its rows only.
 template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ dout,
@@ -351,60 +359,96 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
   constexpr int U = kGatherUnroll;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
-  const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+  const int Wp = (g.W + 1) / 2;  // voxel pairs per grid row
+  const int Np = g.T * g.H * Wp;
+  const int tiles_per_bh = (Np + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   const uint32_t tok_bytes = (uint32_t)g.heads * LY::kRowBytes;  // one token's rows, all heads
 
   for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int n = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
-    if (n >= g.N) continue;
+    const int np = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
+    if (np >= Np) continue;
     const int64_t head_off = ((int64_t)b * g.N * g.heads + m) * LY::kRowBytes + sub * 16;
     const char* qh = static_cast<const char*>(q) + head_off;
     const char* gh = static_cast<const char*>(dout) + head_off;
-    const int x = n % g.W, y = (n / g.W) % g.H, z = n / (g.W * g.H);
-    const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
-    float ak[VEC], av[VEC];
+    const int x0 = 2 * (np % Wp), y = (np / Wp) % g.H, z = np / (Wp * g.H);
+    const bool has1 = x0 + 1 < g.W;
+    float a0k[VEC], a0v[VEC], a1k[VEC], a1v[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
-      ak[e] = 0.0f;
-      av[e] = 0.0f;
+      a0k[e] = 0.0f;
+      a0v[e] = 0.0f;
+      a1k[e] = 0.0f;
+      a1v[e] = 0.0f;
     }
-    // This voxel is corner (cx, cy, cz) of the points whose cell is voxel - (cx, cy, cz).
-    // For each (cy, cz), the bins of cells x-1 (corner cx = 1) and x (cx = 0) are adjacent.
 #pragma unroll 1
     for (int r = 0; r < 4; ++r) {
       const int cy = r & 1, cz = r >> 1;
-      const int64_t ci = cell_index(g, bh, x - 1, y - cy, z - cz);
-      const uint32_t s0 = starts[ci], mid = starts[ci + 1], end = starts[ci + 2];
-      for (uint32_t u = s0; u < end; u += U) {
-        Entry en[U];
-        uint4 qr[U], gr[U];
+      const int64_t ci = cell_index(g, bh, x0 - 1, y - cy, z - cz);
+      const uint32_t s0 = starts[ci], m1 = starts[ci + 1], m2 = starts[ci + 2];
+      const uint32_t end = has1 ? starts[ci + 3] : m2;
+      if (s0 >= end) continue;
+      Entry en[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) en[k] = entries[min(u + k, end - 1)];
+      for (int k = 0; k < U; ++k) en[k] = entries[min(s0 + k, end - 1)];
+      for (uint32_t u = s0; u < end; u += U) {
+        uint4 qr[U], gr[U];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
           const uint64_t o = (uint64_t)(uint32_t)en[k].n * tok_bytes;
           qr[k] = *reinterpret_cast<const uint4*>(qh + o);
           gr[k] = *reinterpret_cast<const uint4*>(gh + o);
         }
+        Entry nx[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) nx[k] = entries[min(u + U + k, end - 1)];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          const bool upper_x = (u + k) < mid;  // entry from cell x-1: this voxel is its cx = 1
-          float w = (upper_x ? en[k].fx : 1.0f - en[k].fx) * (cy ? en[k].fy : 1.0f - en[k].fy) *
-                    (cz ? en[k].fz : 1.0f - en[k].fz);
-          w = (u + k < end) ? w : 0.0f;
-          chunk_axpy<BF16>(ak, en[k].sds * w, qr[k]);
-          chunk_axpy<BF16>(av, en[k].alpha * w, gr[k]);
+          const uint32_t uk = u + k;
+          const float wyz = (uk < end) ? (cy ? en[k].fy : 1.0f - en[k].fy) *
+                                             (cz ? en[k].fz : 1.0f - en[k].fz)
+                                       : 0.0f;
+          const float lo = (1.0f - en[k].fx) * wyz, hi = en[k].fx * wyz;
+          // cell x0-1: x0 is its upper x corner; cell x0: lower for x0, upper for x0+1;
+          // cell x0+1: lower for x0+1
+          const float w0 = uk < m1 ? hi : (uk < m2 ? lo : 0.0f);
+          const float w1 = uk < m1 ? 0.0f : (uk < m2 ? hi : lo);
+          float qf[VEC], gf[VEC];
+          chunk_to_float<BF16>(qr[k], qf);
+          chunk_to_float<BF16>(gr[k], gf);
+          const float k0 = en[k].sds * w0, k1 = en[k].sds * w1;
+          const float v0 = en[k].alpha * w0, v1 = en[k].alpha * w1;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            a0k[e] = fmaf(k0, qf[e], a0k[e]);
+            a1k[e] = fmaf(k1, qf[e], a1k[e]);
+            a0v[e] = fmaf(v0, gf[e], a0v[e]);
+            a1v[e] = fmaf(v1, gf[e], a1v[e]);
+          }
         }
+#pragma unroll
+        for (int k = 0; k < U; ++k) en[k] = nx[k];
       }
     }
-    float* dkr = dk + row * D + sub * VEC;
-    float* dvr = dv + row * D + sub * VEC;
+    const int64_t row0 = ((int64_t)b * g.N + (int64_t)(z * g.H + y) * g.W + x0) * g.heads + m;
+    float* dk0 = dk + row0 * D + sub * VEC;
+    float* dv0 = dv + row0 * D + sub * VEC;
 #pragma unroll
     for (int e = 0; e < VEC; e += 4) {
-      *reinterpret_cast<float4*>(dkr + e) = make_float4(ak[e], ak[e + 1], ak[e + 2], ak[e + 3]);
-      *reinterpret_cast<float4*>(dvr + e) = make_float4(av[e], av[e + 1], av[e + 2], av[e + 3]);
+      *reinterpret_cast<float4*>(dk0 + e) = make_float4(a0k[e], a0k[e + 1], a0k[e + 2], a0k[e + 3]);
+      *reinterpret_cast<float4*>(dv0 + e) = make_float4(a0v[e], a0v[e + 1], a0v[e + 2], a0v[e + 3]);
+    }
+    if (has1) {
+      float* dk1 = dk0 + (int64_t)g.heads * D;
+      float* dv1 = dv0 + (int64_t)g.heads * D;
+#pragma unroll
+      for (int e = 0; e < VEC; e += 4) {
+        *reinterpret_cast<float4*>(dk1 + e) =
+            make_float4(a1k[e], a1k[e + 1], a1k[e + 2], a1k[e + 3]);
+        *reinterpret_cast<float4*>(dv1 + e) =
+            make_float4(a1v[e], a1v[e + 1], a1v[e + 2], a1v[e + 3]);
+      }
     }
   }
 }
@@ -416,7 +460,7 @@ struct Workspace {
   uint32_t* starts;   // [cells + 1]
   uint32_t* cursor;   // [cells]
   uint32_t* sums;     // [ceil(cells / kScanBlockItems)]
-  PointRec* recs;     // [rows * P]
+  PointRec* recs;     // [rows * P], 16-byte aligned
   float* delta;       // [rows]
   Entry* entries;     // [rows * P]
   size_t bytes;
@@ -473,9 +517,9 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   const int tiles = tiles_for<D, BF16>(g);
   const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
   {
-    void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,      (void*)&v,       (void*)&off,
-                 (void*)&lse,  (void*)&dout,   (void*)&dq,     (void*)&doff,    (void*)&w.recs,
-                 (void*)&w.delta, (void*)&w.counts, (void*)&tiles};
+    void* a[] = {(void*)&g,   (void*)&q,    (void*)&k,  (void*)&v,      (void*)&off,
+                 (void*)&lse, (void*)&dout, (void*)&dq, (void*)&w.recs, (void*)&w.delta,
+                 (void*)&w.counts, (void*)&tiles};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16>), dim3(blocks),
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
@@ -505,9 +549,13 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     if (e != hipSuccess) return e;
   }
   {
+    using LY = Layout<D, BF16>;
+    const int64_t pairs = (int64_t)g.T * g.H * ((g.W + 1) / 2);
+    const int gtiles = (int)((pairs + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock * g.B * g.heads);
+    const int gblocks = gtiles < kMaxBlocks ? gtiles : kMaxBlocks;
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
-                 (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&tiles};
-    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16>), dim3(blocks),
+                 (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&gtiles};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16>), dim3(gblocks),
                         dim3(kBlockThreads), a, 0, s);
   }
   return e;

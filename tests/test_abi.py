@@ -139,7 +139,7 @@ def test_workspace_size_follows_the_documented_formula():
         cells = d.batch * d.heads * (d.frames + 1) * (d.height + 1) * (d.width + 1)
         ws = dsa.dsa3d_backward_workspace_size(d)
         assert ws % 256 == 0
-        lo = 44 * rows * P + 12 * cells + 4 * rows
+        lo = 56 * rows * P + 12 * cells + 4 * rows
         assert lo <= ws <= lo + 8 * 256 + 4 * (cells // 4096 + 1) + 4
     assert dsa.dsa3d_backward_workspace_size(good_desc(kt=2)) == 0
 
