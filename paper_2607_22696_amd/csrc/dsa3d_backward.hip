@@ -14,19 +14,17 @@
 //       d_offsets[p] = alpha_p (scale (da_p - Delta) A_p + B_p),
 //       A_p = sum_c dw_c/dpos <q, K_c>,  B_p = sum_c dw_c/dpos <dout, V_c>,
 //     so dq is final at the end of the sweep; (alpha_p, da_p, A_p, B_p) go to a 32-byte
-//     record per point (lane k of a row keeps point k of each chunk of L points, and the
-//     row stores the chunk's records as one contiguous block).  Every point is also counted
-//     into the bin of its trilinear cell (the floor of its position) with an integer atomic
-//     whose result is not waited on.
+//     record per point.  Every point is also counted into the bin of its trilinear cell
+//     (the floor of its position) with an integer atomic whose result is not waited on.
 //  2. exclusive scan of the bin counts -> bin starts (and a copy used as fill cursors).
 //  3. finalize (one thread per point): d_offsets from A_p, B_p and the row's Delta; the
 //     point claims a slot of its bin from the cursor and writes its dK/dV coefficients
 //     (scale ds_p, alpha_p) and fractional position there, i.e. sorted by cell.
-//  4. gather (one L-lane group per pair of voxels adjacent along x): a voxel is corner c of
-//     exactly the points whose cell is voxel - c; for the pair these bins form 4 contiguous
-//     runs (cells x0-1, x0, x0+1 are adjacent), and the group accumulates
+//  4. gather (one L-lane group per 2 x 2 block of voxels in a frame): a voxel is corner c
+//     of exactly the points whose cell is voxel - c; for the block these bins form 6
+//     contiguous runs (cells x0-1, x0, x0+1 are adjacent), and the group accumulates
 //     w_c * coefficient * q and * dout rows in registers, then stores the dK and dV rows of
-//     both voxels once.
+//     its voxels once.
 #include "dsa3d_device.h"
 
 namespace dsa3d {
@@ -49,6 +47,11 @@ struct Entry {
 
 static_assert(sizeof(PointRec) == 32 && sizeof(Entry) == 24, "record layout");
 
+// Register budget of the sweep and gather kernels: at head_dim <= 64 (8 rows per wave) three
+// waves per SIMD (at most 168 VGPRs) measured faster than the compiler's own allocation; at
+// head_dim 128 the unconstrained allocation (two waves) is faster.
+#define DSA3D_WAVES_HINT(D) __attribute__((amdgpu_waves_per_eu((D) <= 64 ? 3 : 1)))
+
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
 constexpr int kScanBlockItems = kScanThreads * kScanItems;
@@ -69,8 +72,13 @@ __device__ inline bool cell_inside(const Geometry& g, int x, int y, int z) {
 
 // ---------------------------------------------------------------------------- 1. sweep
 
+// The lanes of a row share each point's coordinate work: in a chunk of L points, lane `sub`
+// forms point chunk + sub (position, corners, weights, cell), counts it into its bin, and
+// the row's lanes pick the corner indices, fractions and cell up with ds_bpermute; the
+// weights are rebuilt from the fractions with the same products.  Lane `sub` also keeps
+// that point's record, and the row stores the chunk's records as one contiguous block.
 template <int D, bool BF16>
-__global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
+__global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
     const float* __restrict__ offsets, const float* __restrict__ lse,
     const void* __restrict__ dout, float* __restrict__ dq, PointRec* __restrict__ recs,
@@ -88,6 +96,7 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
   const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   const int HW = g.H * g.W;
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
+  const int khw = g.kh * g.kw;
 
   for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
@@ -95,8 +104,8 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
     const int n0 = (tile % tiles_per_bh) * LY::kRowsPerBlock;
     const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, n0 / HW);
     const int n = n0 + wave * LY::kGroups + grp;
-    // All lanes of a group share n: a whole group is idle or active, so the group
-    // reductions never mix an idle group into an active one.
+    // All lanes of a group share n: a whole group is idle or active, so neither the group
+    // reductions nor the point sharing ever mix an idle group into an active one.
     if (n >= g.N) continue;
     const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
@@ -105,7 +114,6 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
     const uint4 gr = load16(gb, row * LY::kRowBytes + lane_off);
     const float lse2 = lse[row] * kLog2e;
     const float* off = offsets + row * g.P * 3;
-    float ox = off[0], oy = off[1], oz = off[2];
     float ak[VEC], bk[VEC];
 #pragma unroll
     for (int x = 0; x < VEC; ++x) {
@@ -113,78 +121,96 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_sweep_kernel(
       bk[x] = 0.0f;
     }
     float delta = 0.0f;
-    float4 rec[2];
 
-    int it = 0, ih = 0, iw = 0;
-    for (int p = 0; p < g.P; ++p) {
-      Point pt;
-      make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, pt);
-      if (p + 1 < g.P) {  // next point's offsets, in flight with this point's corner rows
-        ox = off[3 * p + 3];
-        oy = off[3 * p + 4];
-        oz = off[3 * p + 5];
-      }
-      uint4 kr[8], vr[8];
-      load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
-      float sp = 0.0f, dap = 0.0f;
-      float a3[3] = {0.0f, 0.0f, 0.0f}, b3[3] = {0.0f, 0.0f, 0.0f};
-      float kp[VEC];
-#pragma unroll
-      for (int x = 0; x < VEC; ++x) kp[x] = 0.0f;
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
-        const float qk = chunk_dot<BF16>(qr, kr[c]);
-        const float dvv = chunk_dot<BF16>(gr, vr[c]);
-        sp = fmaf(pt.w[c], qk, sp);
-        dap = fmaf(pt.w[c], dvv, dap);
-        // d w_c / d pos along each axis (corners outside the grid have zero rows, so zero dots)
-        const float wx = cx ? pt.ay[cy] * pt.az[cz] : -(pt.ay[cy] * pt.az[cz]);
-        const float wy = cy ? pt.ax[cx] * pt.az[cz] : -(pt.ax[cx] * pt.az[cz]);
-        const float wz = cz ? pt.ax[cx] * pt.ay[cy] : -(pt.ax[cx] * pt.ay[cy]);
-        a3[0] = fmaf(wx, qk, a3[0]);
-        a3[1] = fmaf(wy, qk, a3[1]);
-        a3[2] = fmaf(wz, qk, a3[2]);
-        b3[0] = fmaf(wx, dvv, b3[0]);
-        b3[1] = fmaf(wy, dvv, b3[1]);
-        b3[2] = fmaf(wz, dvv, b3[2]);
-        chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
-      }
-      const float alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
-      const float da = group_sum<L>(dap);
-      delta = fmaf(alpha, da, delta);
-      const float ada = alpha * da;
-#pragma unroll
-      for (int x = 0; x < VEC; ++x) {
-        ak[x] = fmaf(ada, kp[x], ak[x]);
-        bk[x] = fmaf(alpha, kp[x], bk[x]);
-      }
-#pragma unroll
-      for (int a = 0; a < 3; ++a) {
-        a3[a] = group_sum<L>(a3[a]);
-        b3[a] = group_sum<L>(b3[a]);
-      }
-      if (sub == 0 && cell_inside(g, pt.cx, pt.cy, pt.cz))  // result unused: no wait
-        __hip_atomic_fetch_add(counts + cell_index(g, bh, pt.cx, pt.cy, pt.cz), 1u,
+    int pm = min(sub, g.P - 1);  // this lane's point of the chunk (clamped in the last one)
+    float ox = off[3 * pm], oy = off[3 * pm + 1], oz = off[3 * pm + 2];
+    for (int p0 = 0; p0 < g.P; p0 += L) {
+      const int it = pm / khw, ih = (pm - it * khw) / g.kw, iw = pm - it * khw - ih * g.kw;
+      Point mine;
+      make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
+      const bool own = p0 + sub < g.P;
+      if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))  // result unused: no wait
+        __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      // lane (p mod L) of the row keeps this point's record; one store per chunk of L points
-      if (sub == p % L) {
-        rec[0] = make_float4(alpha, da, a3[0], a3[1]);
-        rec[1] = make_float4(a3[2], b3[0], b3[1], b3[2]);
-      }
-      if (p % L == L - 1 || p == g.P - 1) {
-        if (sub <= p % L) {
-          float4* dst = reinterpret_cast<float4*>(recs + row * g.P + (p - p % L) + sub);
-          dst[0] = rec[0];
-          dst[1] = rec[1];
+      pm = min(p0 + L + sub, g.P - 1);  // next chunk's offsets, in flight during this one
+      ox = off[3 * pm];
+      oy = off[3 * pm + 1];
+      oz = off[3 * pm + 2];
+      const int nk = min(L, g.P - p0);
+      float4 rec0 = make_float4(0.0f, 0.0f, 0.0f, 0.0f), rec1 = rec0;
+      for (int kk = 0; kk < nk; ++kk) {
+        const int src = (grp * L + kk) << 2;
+        Point pt;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) pt.vidx[c] = __builtin_amdgcn_ds_bpermute(src, mine.vidx[c]);
+        const float tx = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.ax[1])));
+        const float ty = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.ay[1])));
+        const float tz = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.az[1])));
+        pt.cx = __builtin_amdgcn_ds_bpermute(src, mine.cx);
+        pt.cy = __builtin_amdgcn_ds_bpermute(src, mine.cy);
+        pt.cz = __builtin_amdgcn_ds_bpermute(src, mine.cz);
+        pt.slow = __builtin_amdgcn_ds_bpermute(src, (int)mine.slow) != 0;
+        pt.ax[0] = 1.0f - tx;
+        pt.ax[1] = tx;
+        pt.ay[0] = 1.0f - ty;
+        pt.ay[1] = ty;
+        pt.az[0] = 1.0f - tz;
+        pt.az[1] = tz;
+        {
+          const float wyz[4] = {pt.ay[0] * pt.az[0], pt.ay[1] * pt.az[0], pt.ay[0] * pt.az[1],
+                                pt.ay[1] * pt.az[1]};
+#pragma unroll
+          for (int c = 0; c < 8; ++c) pt.w[c] = pt.ax[c & 1] * wyz[c >> 1];
+        }
+        uint4 kr[8], vr[8];
+        load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
+        float sp = 0.0f, dap = 0.0f;
+        float a3[3] = {0.0f, 0.0f, 0.0f}, b3[3] = {0.0f, 0.0f, 0.0f};
+        float kp[VEC];
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) kp[x] = 0.0f;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
+          const float qk = chunk_dot<BF16>(qr, kr[c]);
+          const float dvv = chunk_dot<BF16>(gr, vr[c]);
+          sp = fmaf(pt.w[c], qk, sp);
+          dap = fmaf(pt.w[c], dvv, dap);
+          // d w_c / d pos along each axis (corners outside the grid have zero rows, so zero dots)
+          const float wx = cx ? pt.ay[cy] * pt.az[cz] : -(pt.ay[cy] * pt.az[cz]);
+          const float wy = cy ? pt.ax[cx] * pt.az[cz] : -(pt.ax[cx] * pt.az[cz]);
+          const float wz = cz ? pt.ax[cx] * pt.ay[cy] : -(pt.ax[cx] * pt.ay[cy]);
+          a3[0] = fmaf(wx, qk, a3[0]);
+          a3[1] = fmaf(wy, qk, a3[1]);
+          a3[2] = fmaf(wz, qk, a3[2]);
+          b3[0] = fmaf(wx, dvv, b3[0]);
+          b3[1] = fmaf(wy, dvv, b3[1]);
+          b3[2] = fmaf(wz, dvv, b3[2]);
+          chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
+        }
+        const float alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
+        const float da = group_sum<L>(dap);
+        delta = fmaf(alpha, da, delta);
+        const float ada = alpha * da;
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) {
+          ak[x] = fmaf(ada, kp[x], ak[x]);
+          bk[x] = fmaf(alpha, kp[x], bk[x]);
+        }
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+          a3[a] = group_sum<L>(a3[a]);
+          b3[a] = group_sum<L>(b3[a]);
+        }
+        if (sub == kk) {
+          rec0 = make_float4(alpha, da, a3[0], a3[1]);
+          rec1 = make_float4(a3[2], b3[0], b3[1], b3[2]);
         }
       }
-      if (++iw == g.kw) {
-        iw = 0;
-        if (++ih == g.kh) {
-          ih = 0;
-          ++it;
-        }
+      if (own) {
+        float4* dst = reinterpret_cast<float4*>(recs + row * g.P + p0 + sub);
+        dst[0] = rec0;
+        dst[1] = rec1;
       }
     }
     float* dqr = dq + row * D + sub * VEC;
@@ -342,112 +368,148 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
 
 constexpr int kGatherUnroll = 4;  // bin entries processed per iteration
 
-// Each L-lane group owns two voxels adjacent along x, (x0, x0 + 1).  For a (cy, cz) corner
-// pair, the voxels are corners of the points in cells x0-1 (x0 only, as cx = 1), x0 (both:
-// cx = 0 for x0, cx = 1 for x0 + 1) and x0+1 (x0 + 1 only, as cx = 0); those three bins are
-// adjacent, so one contiguous run of entries serves both voxels and every entry's q and dout
-// rows are loaded once for the pair.  Entries are read one batch ahead, so a batch waits for
-// its rows only.
+// Per-lane dK/dV accumulators of a group's 2 x 2 voxel block: voxel v = 2 * yi + xi.
+template <int VEC>
+struct BlockAcc {
+  float k[4][VEC];
+  float v[4][VEC];
+};
+
+// One run of bins: the cells (x0 - 1, x0, x0 + 1) of cell row y0 - 1 + YR in one z plane,
+// contiguous in the bin order.  Cell row y0 - 1 feeds voxel row y0 (as its upper y corner),
+// cell row y0 feeds both rows (lower corner of y0, upper of y0 + 1) and cell row y0 + 1 feeds
+// row y0 + 1 (as its lower corner); YR is the same for every group of a wave, so each case is
+// its own code and a run touches only the accumulators of the rows it feeds.  Along x the
+// voxel x0 is the upper corner of cell x0 - 1 and the lower of cell x0, the voxel x0 + 1 the
+// upper of x0 and the lower of x0 + 1: [s0, m1), [m1, m2), [m2, end).  `zlow` says whether
+// the voxels are the lower z corner of this plane's cells.  Entries are read one batch
+// ahead, so a batch waits for its rows only.
+template <int D, bool BF16, int YR>
+__device__ inline __attribute__((always_inline)) void gather_run(
+    const char* __restrict__ qh, const char* __restrict__ gh, uint32_t tok_bytes,
+    const Entry* __restrict__ entries, uint32_t s0, uint32_t m1, uint32_t m2, uint32_t end,
+    bool zlow, BlockAcc<Layout<D, BF16>::kVec>& acc) {
+  using LY = Layout<D, BF16>;
+  constexpr int VEC = LY::kVec;
+  constexpr int U = kGatherUnroll;
+  if (s0 >= end) return;
+  Entry en[U];
+#pragma unroll
+  for (int k = 0; k < U; ++k) en[k] = entries[min(s0 + k, end - 1)];
+  for (uint32_t u = s0; u < end; u += U) {
+    uint4 qr[U], gr[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint64_t o = (uint64_t)(uint32_t)en[k].n * tok_bytes;
+      qr[k] = *reinterpret_cast<const uint4*>(qh + o);
+      gr[k] = *reinterpret_cast<const uint4*>(gh + o);
+    }
+    Entry nx[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) nx[k] = entries[min(u + U + k, end - 1)];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint32_t uk = u + k;
+      const float wz = uk < end ? (zlow ? 1.0f - en[k].fz : en[k].fz) : 0.0f;
+      const float lo = 1.0f - en[k].fx;
+      const float tx0 = wz * (uk < m1 ? en[k].fx : (uk < m2 ? lo : 0.0f));
+      const float tx1 = wz * (uk < m1 ? 0.0f : (uk < m2 ? en[k].fx : lo));
+      float qf[VEC], gf[VEC];
+      chunk_to_float<BF16>(qr[k], qf);
+      chunk_to_float<BF16>(gr[k], gf);
+#pragma unroll
+      for (int yi = 0; yi < 2; ++yi) {
+        if ((YR == 0 && yi == 1) || (YR == 2 && yi == 0)) continue;
+        // lower y corner for (YR, yi) = (1, 0), (2, 1); upper for (0, 0), (1, 1)
+        const float wy = (YR - yi == 1) ? 1.0f - en[k].fy : en[k].fy;
+        const float sk = en[k].sds * wy, sv = en[k].alpha * wy;
+        const float k0 = sk * tx0, k1 = sk * tx1, v0 = sv * tx0, v1 = sv * tx1;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          acc.k[2 * yi][e] = fmaf(k0, qf[e], acc.k[2 * yi][e]);
+          acc.k[2 * yi + 1][e] = fmaf(k1, qf[e], acc.k[2 * yi + 1][e]);
+          acc.v[2 * yi][e] = fmaf(v0, gf[e], acc.v[2 * yi][e]);
+          acc.v[2 * yi + 1][e] = fmaf(v1, gf[e], acc.v[2 * yi + 1][e]);
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) en[k] = nx[k];
+  }
+}
+
+// Each L-lane group owns the 2 x 2 block of voxels (x0..x0+1, y0..y0+1) of one frame z.  The
+// block's voxels are corners of the points in the 3 x 3 cells (x0-1..x0+1, y0-1..y0+1) of
+// the planes z - 1 and z: six runs of three adjacent bins, and each entry's q and dout rows
+// are loaded once per run for all the voxels it feeds.
 template <int D, bool BF16>
-__global__ __launch_bounds__(kBlockThreads) void bwd_gather_kernel(
+__global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ dout,
     const uint32_t* __restrict__ starts, const Entry* __restrict__ entries, float* __restrict__ dk,
     float* __restrict__ dv, int tiles) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
-  constexpr int U = kGatherUnroll;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
-  const int Wp = (g.W + 1) / 2;  // voxel pairs per grid row
-  const int Np = g.T * g.H * Wp;
-  const int tiles_per_bh = (Np + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
+  const int Wb = (g.W + 1) / 2, Hb = (g.H + 1) / 2;  // blocks per grid row / column
+  const int Nb = g.T * Hb * Wb;
+  const int tiles_per_bh = (Nb + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   const uint32_t tok_bytes = (uint32_t)g.heads * LY::kRowBytes;  // one token's rows, all heads
 
   for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int np = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
-    if (np >= Np) continue;
+    const int nb = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
+    if (nb >= Nb) continue;
     const int64_t head_off = ((int64_t)b * g.N * g.heads + m) * LY::kRowBytes + sub * 16;
     const char* qh = static_cast<const char*>(q) + head_off;
     const char* gh = static_cast<const char*>(dout) + head_off;
-    const int x0 = 2 * (np % Wp), y = (np / Wp) % g.H, z = np / (Wp * g.H);
-    const bool has1 = x0 + 1 < g.W;
-    float a0k[VEC], a0v[VEC], a1k[VEC], a1v[VEC];
+    const int x0 = 2 * (nb % Wb), y0 = 2 * ((nb / Wb) % Hb), z = nb / (Wb * Hb);
+    const bool hasx1 = x0 + 1 < g.W, hasy1 = y0 + 1 < g.H;
+    BlockAcc<VEC> acc;
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      a0k[e] = 0.0f;
-      a0v[e] = 0.0f;
-      a1k[e] = 0.0f;
-      a1v[e] = 0.0f;
-    }
-#pragma unroll 1
-    for (int r = 0; r < 4; ++r) {
-      const int cy = r & 1, cz = r >> 1;
-      const int64_t ci = cell_index(g, bh, x0 - 1, y - cy, z - cz);
-      const uint32_t s0 = starts[ci], m1 = starts[ci + 1], m2 = starts[ci + 2];
-      const uint32_t end = has1 ? starts[ci + 3] : m2;
-      if (s0 >= end) continue;
-      Entry en[U];
+    for (int c = 0; c < 4; ++c) {
 #pragma unroll
-      for (int k = 0; k < U; ++k) en[k] = entries[min(s0 + k, end - 1)];
-      for (uint32_t u = s0; u < end; u += U) {
-        uint4 qr[U], gr[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const uint64_t o = (uint64_t)(uint32_t)en[k].n * tok_bytes;
-          qr[k] = *reinterpret_cast<const uint4*>(qh + o);
-          gr[k] = *reinterpret_cast<const uint4*>(gh + o);
-        }
-        Entry nx[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k) nx[k] = entries[min(u + U + k, end - 1)];
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const uint32_t uk = u + k;
-          const float wyz = (uk < end) ? (cy ? en[k].fy : 1.0f - en[k].fy) *
-                                             (cz ? en[k].fz : 1.0f - en[k].fz)
-                                       : 0.0f;
-          const float lo = (1.0f - en[k].fx) * wyz, hi = en[k].fx * wyz;
-          // cell x0-1: x0 is its upper x corner; cell x0: lower for x0, upper for x0+1;
-          // cell x0+1: lower for x0+1
-          const float w0 = uk < m1 ? hi : (uk < m2 ? lo : 0.0f);
-          const float w1 = uk < m1 ? 0.0f : (uk < m2 ? hi : lo);
-          float qf[VEC], gf[VEC];
-          chunk_to_float<BF16>(qr[k], qf);
-          chunk_to_float<BF16>(gr[k], gf);
-          const float k0 = en[k].sds * w0, k1 = en[k].sds * w1;
-          const float v0 = en[k].alpha * w0, v1 = en[k].alpha * w1;
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            a0k[e] = fmaf(k0, qf[e], a0k[e]);
-            a1k[e] = fmaf(k1, qf[e], a1k[e]);
-            a0v[e] = fmaf(v0, gf[e], a0v[e]);
-            a1v[e] = fmaf(v1, gf[e], a1v[e]);
-          }
-        }
-#pragma unroll
-        for (int k = 0; k < U; ++k) en[k] = nx[k];
+      for (int e = 0; e < VEC; ++e) {
+        acc.k[c][e] = 0.0f;
+        acc.v[c][e] = 0.0f;
       }
     }
-    const int64_t row0 = ((int64_t)b * g.N + (int64_t)(z * g.H + y) * g.W + x0) * g.heads + m;
-    float* dk0 = dk + row0 * D + sub * VEC;
-    float* dv0 = dv + row0 * D + sub * VEC;
+#pragma unroll 1
+    for (int cz = 0; cz < 2; ++cz) {  // cell plane z - 1 + cz; voxel z is its upper corner for cz = 0
+      uint32_t r[3][4];
 #pragma unroll
-    for (int e = 0; e < VEC; e += 4) {
-      *reinterpret_cast<float4*>(dk0 + e) = make_float4(a0k[e], a0k[e + 1], a0k[e + 2], a0k[e + 3]);
-      *reinterpret_cast<float4*>(dv0 + e) = make_float4(a0v[e], a0v[e + 1], a0v[e + 2], a0v[e + 3]);
+      for (int yr = 0; yr < 3; ++yr) {
+        if (yr == 2 && !hasy1) {  // cell row y0 + 1 is outside the cell grid: nothing to gather
+          r[yr][0] = r[yr][1] = r[yr][2] = r[yr][3] = 0u;
+          continue;
+        }
+        const int64_t ci = cell_index(g, bh, x0 - 1, y0 - 1 + yr, z - 1 + cz);
+        r[yr][0] = starts[ci];
+        r[yr][1] = starts[ci + 1];
+        r[yr][2] = starts[ci + 2];
+        r[yr][3] = hasx1 ? starts[ci + 3] : r[yr][2];
+      }
+      const bool zlow = cz == 1;
+      gather_run<D, BF16, 0>(qh, gh, tok_bytes, entries, r[0][0], r[0][1], r[0][2], r[0][3], zlow, acc);
+      gather_run<D, BF16, 1>(qh, gh, tok_bytes, entries, r[1][0], r[1][1], r[1][2], r[1][3], zlow, acc);
+      gather_run<D, BF16, 2>(qh, gh, tok_bytes, entries, r[2][0], r[2][1], r[2][2], r[2][3], zlow, acc);
     }
-    if (has1) {
-      float* dk1 = dk0 + (int64_t)g.heads * D;
-      float* dv1 = dv0 + (int64_t)g.heads * D;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int xi = c & 1, yi = c >> 1;
+      if ((xi == 1 && !hasx1) || (yi == 1 && !hasy1)) continue;
+      const int64_t row =
+          ((int64_t)b * g.N + (int64_t)(z * g.H + y0 + yi) * g.W + x0 + xi) * g.heads + m;
+      float* dkr = dk + row * D + sub * VEC;
+      float* dvr = dv + row * D + sub * VEC;
 #pragma unroll
       for (int e = 0; e < VEC; e += 4) {
-        *reinterpret_cast<float4*>(dk1 + e) =
-            make_float4(a1k[e], a1k[e + 1], a1k[e + 2], a1k[e + 3]);
-        *reinterpret_cast<float4*>(dv1 + e) =
-            make_float4(a1v[e], a1v[e + 1], a1v[e + 2], a1v[e + 3]);
+        *reinterpret_cast<float4*>(dkr + e) =
+            make_float4(acc.k[c][e], acc.k[c][e + 1], acc.k[c][e + 2], acc.k[c][e + 3]);
+        *reinterpret_cast<float4*>(dvr + e) =
+            make_float4(acc.v[c][e], acc.v[c][e + 1], acc.v[c][e + 2], acc.v[c][e + 3]);
       }
     }
   }
@@ -550,8 +612,8 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   }
   {
     using LY = Layout<D, BF16>;
-    const int64_t pairs = (int64_t)g.T * g.H * ((g.W + 1) / 2);
-    const int gtiles = (int)((pairs + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock * g.B * g.heads);
+    const int64_t vblocks = (int64_t)g.T * ((g.H + 1) / 2) * ((g.W + 1) / 2);
+    const int gtiles = (int)((vblocks + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock * g.B * g.heads);
     const int gblocks = gtiles < kMaxBlocks ? gtiles : kMaxBlocks;
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
                  (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&gtiles};
