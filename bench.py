@@ -42,25 +42,25 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def kernel_family(name: str) -> str:
-    """Which entry point a kernel of the library belongs to."""
-    return "forward" if "fwd_kernel" in name else "backward"
+def kernel_base(name: str) -> str:
+    """Kernel function name without namespace, template arguments or parameters."""
+    import re
+    m = re.search(r"(\w+_kernel)\b|(__amd_rocclr_copyBuffer)", name)
+    return m.group(0) if m else name[:60]
 
 
 def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
     """Turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE of the bench command, and of
-    a device copy of copy_mib MiB) into profiles/traffic_<workload>.json: HBM bytes per call of
-    each entry point, each counter scaled by what it reads for the copy of known size."""
+    a device copy of copy_mib MiB) into profiles/traffic_<workload>.json: HBM bytes per
+    launch of each kernel, each counter scaled by what it reads for the copy of known size."""
     import csv
-    import re
 
     def per_kernel(d):
         path = [os.path.join(d, f) for f in os.listdir(d) if f.endswith("counter_collection.csv")][0]
         acc = {}
         for r in csv.DictReader(open(path)):
-            m = re.search(r"(\w+_kernel)(<[^>]*>)?|(__amd_rocclr_copyBuffer)", r["Kernel_Name"])
-            key = m.group(0) if m else r["Kernel_Name"][:60]
-            acc.setdefault(key, []).append(float(r["Counter_Value"]) * 1024.0)  # KiB -> B
+            acc.setdefault(kernel_base(r["Kernel_Name"]), []).append(
+                float(r["Counter_Value"]) * 1024.0)  # KiB -> B
         return acc
 
     fetch, write = per_kernel(fetch_dir), per_kernel(write_dir)
@@ -71,14 +71,14 @@ def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
     write_scale = (sum(cw) / len(cw)) / true_bytes
     out = {"workload": workload, "kernel_source_hash": kernel_source_hash(),
            "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
-           "kernels": {}, "per_call_bytes": {"forward": 0.0, "backward": 0.0}}
+           "kernels": {}}
     for k in fetch:
         if k not in write or k == "__amd_rocclr_copyBuffer":
             continue
         f = sum(fetch[k]) / len(fetch[k]) / fetch_scale
         w = sum(write[k]) / len(write[k]) / write_scale
-        out["kernels"][k] = {"fetch_bytes": round(f), "write_bytes": round(w)}
-        out["per_call_bytes"][kernel_family(k)] += f + w
+        out["kernels"][k] = {"fetch_bytes": round(f), "write_bytes": round(w),
+                             "hbm_bytes": round(f + w)}
     os.makedirs(PROFILES, exist_ok=True)
     path = os.path.join(PROFILES, f"traffic_{workload}.json")
     with open(path, "w") as fh:
@@ -86,8 +86,9 @@ def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
     print(path)
 
 
-def measured_traffic(workload, kernel_name):
-    """HBM bytes per call from profiles/traffic_<workload>.json, or None if absent or stale."""
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from profiles/traffic_<workload>.json, or None if
+    absent or taken from other kernel sources."""
     path = os.path.join(PROFILES, f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
@@ -95,58 +96,90 @@ def measured_traffic(workload, kernel_name):
         d = json.load(fh)
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return d["per_call_bytes"].get(kernel_name)
+    k = d.get("kernels", {}).get(kernel)
+    return None if k is None else k["hbm_bytes"]
 
 
 def algorithmic(w):
-    """Per-launch algorithmic HBM bytes and FLOPs of the forward and backward kernels.
+    """Algorithmic HBM bytes and FLOPs per launch of each kernel, and of the two entry points.
 
-    Per query row (token, head), with s = bytes per q/k/v element:
-      forward  bytes  q, k, v read + out written (4 D s) + offsets (12 P) + lse (4)
-               flops  16 P D multiply-adds (8 corners x D for q.K, 8 x D for V) = 32 P D
-      backward bytes  q, k, v, dout read (4 D s) + offsets (12 P) + lse (4)
-                      + dq, dk, dv written (3 D 4) + d_offsets (12 P)
-               flops  40 P D multiply-adds (q.K, dout.V, dq, dK scatter, dV scatter) = 80 P D
+    Per query row (token, head), with s = bytes per q/k/v element, P points, head_dim D:
+      fwd_kernel           bytes  q, k, v read + out written (4 D s), offsets (12 P), lse (4)
+                           flops  16 P D multiply-adds: 8 corners x D for q.K, 8 x D for V
+      bwd_sweep_kernel     bytes  q, k, v, dout read (4 D s), offsets (12 P), lse (4), dq (4 D)
+                           flops  24 P D multiply-adds: q.K_c and dout.V_c at 8 corners, and
+                                  the 8-corner K interpolation that dq needs
+      bwd_finalize_kernel  bytes  offsets read (12 P), d_offsets written (12 P)
+      bwd_gather_kernel    bytes  q, dout read (2 D s), dk, dv written (8 D)
+                           flops  16 P D multiply-adds: w_c ds_p q into dK and w_c alpha_p dout
+                                  into dV at 8 corners
+      backward (entry)     bytes  q, k, v, dout (4 D s), offsets (12 P), lse (4) read once;
+                                  dq, dk, dv (12 D) and d_offsets (12 P) written once
+                           flops  40 P D multiply-adds
+    A multiply-add is 2 FLOPs.  The bin scan moves 4-byte counters only (no algorithmic work).
     """
     s = 2 if w.dtype == "bf16" else 4
     rows = w.queries
     P, D = w.P, w.head_dim
-    return {
-        "fwd_bytes": rows * (4 * D * s + 12 * P + 4),
-        "fwd_flops": rows * 32 * P * D,
-        "bwd_bytes": rows * (4 * D * s + 12 * P + 4 + 3 * D * 4 + 12 * P),
-        "bwd_flops": rows * 80 * P * D,
+    per = {
+        "fwd_kernel": (4 * D * s + 12 * P + 4, 32 * P * D),
+        "bwd_sweep_kernel": (4 * D * s + 12 * P + 4 + 4 * D, 48 * P * D),
+        "bwd_finalize_kernel": (24 * P, 0),
+        "bwd_gather_kernel": (2 * D * s + 8 * D, 32 * P * D),
+        "forward": (4 * D * s + 12 * P + 4, 32 * P * D),
+        "backward": (4 * D * s + 12 * P + 4 + 3 * D * 4 + 12 * P, 80 * P * D),
     }
+    return {k: {"bytes": rows * b, "flops": rows * f} for k, (b, f) in per.items()}
+
+
+def roofline(work, ms):
+    """Roofline entry of one kernel: bound by whichever of HBM bytes and fp32 VALU flops takes
+    longer at peak; achieved = algorithmic work per launch / average launch time."""
+    t_hbm = work["bytes"] / (HBM_PEAK_GBS * 1e9)
+    t_alu = work["flops"] / (VALU_PEAK_TFLOPS * 1e12)
+    if t_alu >= t_hbm:
+        ach = work["flops"] / (ms * 1e-3) / 1e12
+        return {"bound": "alu", "achieved": round(ach, 3), "peak": VALU_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / VALU_PEAK_TFLOPS, 4)}
+    ach = work["bytes"] / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBS, 4)}
 
 
 def cpu_baseline(w, host, budget_s, backward=True):
     """The oracle (forward rows, plus the backward slab with its dK/dV scatter when the step
-    has a backward) on head 0, one frame at a time, until about budget_s seconds of CPU work;
-    reported in query tokens per second."""
+    has a backward) one (head, frame) at a time, head 0 first, until about budget_s seconds
+    of CPU work; reported in query tokens per second."""
     import numpy as np
 
     import oracle
     q, k, v, off, dout = host
     shape = (w.B, w.T, w.H, w.W, w.heads, w.head_dim, w.kt, w.kh, w.kw)
     HW = w.H * w.W
-    dk = np.zeros((w.T, w.H, w.W, w.head_dim)) if backward else None
-    dv = np.zeros_like(dk) if backward else None
     rows_done = 0
-    frames = 0
+    done = []  # (head, frames) per head touched
     t0 = time.perf_counter()
-    while frames < w.T and time.perf_counter() - t0 < budget_s:
-        rows = (np.arange(HW, dtype=np.int64) + frames * HW) * w.heads  # head 0 of each token
-        oracle.forward(shape, w.dtype, q, k, v, off, rows=rows)
-        if backward:
-            oracle.backward_slab(shape, w.dtype, q, k, v, off, dout, 0, 0, frames, frames + 1,
-                                 dk=dk, dv=dv)
-        rows_done += HW
-        frames += 1
+    for m in range(w.heads):
+        if time.perf_counter() - t0 >= budget_s:
+            break
+        dk = np.zeros((w.T, w.H, w.W, w.head_dim)) if backward else None
+        dv = np.zeros_like(dk) if backward else None
+        frames = 0
+        while frames < w.T and time.perf_counter() - t0 < budget_s:
+            rows = (np.arange(HW, dtype=np.int64) + frames * HW) * w.heads + m
+            oracle.forward(shape, w.dtype, q, k, v, off, rows=rows)
+            if backward:
+                oracle.backward_slab(shape, w.dtype, q, k, v, off, dout, 0, m, frames,
+                                     frames + 1, dk=dk, dv=dv)
+            rows_done += HW
+            frames += 1
+        done.append((m, frames))
     dt = time.perf_counter() - t0
+    what = ", ".join(f"head {m} frames [0,{f})" for m, f in done)
     # one query token carries all heads: rows / heads tokens
     return {"value": rows_done / w.heads / dt, "unit": "queries/s", "cores": oracle.threads(),
             "kind": "oracle",
-            "sample": f"head 0 of frames [0,{frames}) of {w.name}: {rows_done} (token, head) rows, "
+            "sample": f"{what} of {w.name}: {rows_done} (token, head) rows, "
                       + ("forward + backward incl. dK/dV scatter" if backward else "forward")
                       + f", fp64, {dt:.1f} s; "
                       f"scaled to query tokens (all {w.heads} heads)"}
@@ -218,60 +251,70 @@ def main():
     kern = (w.kt, w.kh, w.kw)
     out, lse = dsa.forward(qd, kd, vd, od, kernel=kern)
     grads = None
+    workspace = None
     if do_bwd:
         f32 = dict(dtype=torch.float32, device=qd.device)
         grads = (torch.empty(q.shape, **f32), torch.empty(q.shape, **f32),
                  torch.empty(q.shape, **f32), torch.empty(off.shape, **f32))
+        need = dsa.dsa3d_backward_workspace_size(dsa.make_desc(
+            w.B, w.T, w.H, w.W, w.heads, w.head_dim, w.kt, w.kh, w.kw, w.dtype))
+        workspace = torch.empty(need, dtype=torch.uint8, device=qd.device)
 
-    def step():
+    def new_events(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:  # create the HIP events before they are handed to the library
+            e.record()
+        return evs
+
+    nph = dsa.DSA3D_BACKWARD_PHASES
+    K = args.steps
+    ev = [new_events(3) for _ in range(K)]
+    ph = [new_events(nph + 1) for _ in range(K)] if do_bwd else None
+
+    def step(s=None):
+        if s is not None:
+            ev[s][0].record()
         dsa.forward(qd, kd, vd, od, kernel=kern, out=out, lse=lse)
+        if s is not None:
+            ev[s][1].record()
         if do_bwd:
-            dsa.backward(qd, kd, vd, od, lse, gd, kernel=kern, grads=grads)
+            dsa.backward(qd, kd, vd, od, lse, gd, kernel=kern, grads=grads, workspace=workspace,
+                         phase_events=None if s is None else ph[s])
+        if s is not None:
+            ev[s][2].record()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for s in range(K):
-        ev[s][0].record()
-        dsa.forward(qd, kd, vd, od, kernel=kern, out=out, lse=lse)
-        ev[s][1].record()
-        if do_bwd:
-            dsa.backward(qd, kd, vd, od, lse, gd, kernel=kern, grads=grads)
-        ev[s][2].record()
+        step(s)
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
     bwd_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / K if do_bwd else 0.0
     ms_step = total_ms / K
+    # average duration of each kernel (HIP events on the stream the kernels run on)
+    kernel_ms = {"fwd_kernel": fwd_ms}
+    if do_bwd:
+        names = ["bwd_sweep_kernel", "bin_scan", "bwd_finalize_kernel", "bwd_gather_kernel"]
+        for i, n in enumerate(names):
+            kernel_ms[n] = sum(p[i].elapsed_time(p[i + 1]) for p in ph) / K
 
     alg = algorithmic(w)
-    step_bytes = alg["fwd_bytes"] + (alg["bwd_bytes"] if do_bwd else 0)
+    step_bytes = alg["forward"]["bytes"] + (alg["backward"]["bytes"] if do_bwd else 0)
     tokens = w.B * w.N
-    # dominant kernel: the longer of the two launches
-    kname, kms = ("backward", bwd_ms) if do_bwd and bwd_ms >= fwd_ms else ("forward", fwd_ms)
-    kbytes = alg["bwd_bytes"] if kname == "backward" else alg["fwd_bytes"]
-    kflops = alg["bwd_flops"] if kname == "backward" else alg["fwd_flops"]
-    t_hbm = kbytes / (HBM_PEAK_GBS * 1e9)
-    t_alu = kflops / (VALU_PEAK_TFLOPS * 1e12)
-    if t_alu >= t_hbm:
-        ach = kflops / (kms * 1e-3) / 1e12
-        roof = {"bound": "alu", "achieved": round(ach, 3), "peak": VALU_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / VALU_PEAK_TFLOPS, 4), "traffic": None}
-    else:
-        ach = kbytes / (kms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+    # dominant kernel: the longest single kernel of the step
+    kname = max((n for n in kernel_ms if n in alg), key=lambda n: kernel_ms[n])
+    roof = roofline(alg[kname], kernel_ms[kname])
     tr = measured_traffic(w.name, kname)
     roof["traffic"] = None if tr is None else round(tr)
-    roof["kernel"] = f"dsa3d_{kname}"
-    roof["avg_launch_ms"] = round(kms, 4)
+    roof["kernel"] = kname
+    roof["avg_launch_ms"] = round(kernel_ms[kname], 4)
 
     res = {
         "metric": METRIC,
@@ -291,6 +334,8 @@ def main():
                    "points": w.P, "backward": do_bwd, "parallelism": "single GPU"},
         "fwd_ms": round(fwd_ms, 4),
         "bwd_ms": round(bwd_ms, 4),
+        "kernel_ms": {n: round(t, 4) for n, t in kernel_ms.items()},
+        "kernel_roofline": {n: roofline(alg[n], t) for n, t in kernel_ms.items() if n in alg},
         "hbm_gbs_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "token_head_rows_per_s": round(w.queries / (ms_step * 1e-3), 1),

@@ -113,9 +113,10 @@ size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc);
  *   dq, d_offsets : fully overwritten.
  *   dk, dv   : fully overwritten.  No floating-point atomics are used: every (row, point)
  *              pair is binned by its trilinear cell and each voxel gathers its gradient
- *              rows from the 8 bins it is a corner of, so results are deterministic up to
- *              the (fixed) order of a bin, which depends on scheduling only through the
- *              integer bin counters.
+ *              rows from the 8 bins it is a corner of.  The order of the pairs inside a bin
+ *              follows the order in which they claimed their slots, which can change from
+ *              call to call, so dk and dv can differ between calls in the last bits
+ *              (dq and d_offsets are bitwise repeatable).
  *   workspace: device memory of at least dsa3d_backward_workspace_size(desc) bytes, 256-byte
  *              aligned, not overlapping any argument; contents on entry do not matter.
  * Additional limit: rows * P and the number of cells, B*heads*(T+1)*(H+1)*(W+1), must be
@@ -125,6 +126,23 @@ dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k
                             const float* offsets, const float* lse, const void* dout, float* dq,
                             float* dk, float* dv, float* d_offsets, void* workspace,
                             size_t workspace_bytes, void* stream);
+
+/* Phases of dsa3d_backward, in launch order: 0 the sweep over query rows (dq, per-point
+ * records, bin counts), 1 the exclusive scan of the bin counts, 2 the pass over points
+ * (d_offsets, binned dK/dV coefficients), 3 the dK/dV gather over voxels. */
+#define DSA3D_BACKWARD_PHASES 4
+
+/* dsa3d_backward with phase timing, for benchmarks and profilers.  `events` is NULL or
+ * points to DSA3D_BACKWARD_PHASES + 1 HIP events (hipEvent_t handles, created by the caller
+ * on the current device and owned by it); event i is recorded on `stream` right before
+ * phase i is launched and the last one after the last phase, so the time between events i
+ * and i + 1 is phase i alone.  Arguments, checks and results are those of dsa3d_backward;
+ * a failed event record returns DSA3D_ERR_DEVICE. */
+dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const void* k,
+                                  const void* v, const float* offsets, const float* lse,
+                                  const void* dout, float* dq, float* dk, float* dv,
+                                  float* d_offsets, void* workspace, size_t workspace_bytes,
+                                  void* stream, void* const* events);
 
 /* Static description of a status code (never NULL). */
 const char* dsa3d_status_string(dsa3d_status status);

@@ -5,7 +5,7 @@ declared in ``include/dsa3d.h``.  This package holds the kernels (``csrc/``), th
 script and a thin binding; PyTorch is used only for device memory and streams.
 """
 from ._binding import (  # noqa: F401
-    DSA3D_BF16, DSA3D_F32, DSA3D_MAX_POINTS, DSA3D_OK, EXPORTED, Dsa3dError, dsa3d_abi_version,
-    dsa3d_backward, dsa3d_backward_workspace_size, dsa3d_desc, dsa3d_forward, load, make_desc,
-    status_string)
+    DSA3D_BACKWARD_PHASES, DSA3D_BF16, DSA3D_F32, DSA3D_MAX_POINTS, DSA3D_OK, EXPORTED, Dsa3dError,
+    dsa3d_abi_version, dsa3d_backward, dsa3d_backward_timed, dsa3d_backward_workspace_size,
+    dsa3d_desc, dsa3d_forward, load, make_desc, status_string)
 from .ops import backward, forward  # noqa: F401

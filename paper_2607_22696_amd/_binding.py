@@ -26,8 +26,10 @@ DSA3D_F32 = 0
 DSA3D_BF16 = 1
 DSA3D_MAX_POINTS = 1024
 
-EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_workspace_size",
-            "dsa3d_status_string", "dsa3d_abi_version")
+DSA3D_BACKWARD_PHASES = 4
+
+EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_timed",
+            "dsa3d_backward_workspace_size", "dsa3d_status_string", "dsa3d_abi_version")
 
 
 class dsa3d_desc(ctypes.Structure):
@@ -60,6 +62,9 @@ def load():
         lib.dsa3d_backward.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ctypes.c_size_t, vp]
         lib.dsa3d_backward.restype = ctypes.c_int
+        lib.dsa3d_backward_timed.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                             ctypes.c_size_t, vp, ctypes.POINTER(vp)]
+        lib.dsa3d_backward_timed.restype = ctypes.c_int
         lib.dsa3d_backward_workspace_size.argtypes = [pd]
         lib.dsa3d_backward_workspace_size.restype = ctypes.c_size_t
         lib.dsa3d_status_string.argtypes = [ctypes.c_int]
@@ -121,6 +126,26 @@ def dsa3d_backward(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets,
                                workspace_bytes, _stream(stream))
     if check and st != DSA3D_OK:
         raise Dsa3dError(st, "dsa3d_backward")
+    return st
+
+
+def dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets,
+                         workspace=None, workspace_bytes=0, stream=None, events=None,
+                         check=True) -> int:
+    """`events`: None or DSA3D_BACKWARD_PHASES + 1 torch.cuda.Event objects (or raw hipEvent_t
+    addresses); each must already be created, i.e. recorded once."""
+    arr = None
+    if events is not None:
+        handles = [e if isinstance(e, int) else e.cuda_event for e in events]
+        if len(handles) != DSA3D_BACKWARD_PHASES + 1 or not all(handles):
+            raise ValueError("dsa3d_backward_timed needs DSA3D_BACKWARD_PHASES + 1 created events")
+        arr = (ctypes.c_void_p * len(handles))(*handles)
+    st = load().dsa3d_backward_timed(ctypes.byref(desc) if desc is not None else None, _ptr(q),
+                                     _ptr(k), _ptr(v), _ptr(offsets), _ptr(lse), _ptr(dout),
+                                     _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_offsets),
+                                     _ptr(workspace), workspace_bytes, _stream(stream), arr)
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_backward_timed")
     return st
 
 

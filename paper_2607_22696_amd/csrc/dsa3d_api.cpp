@@ -148,10 +148,11 @@ size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc) {
   return dsa3d::backward_workspace_bytes(g);
 }
 
-dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
-                            const float* offsets, const float* lse, const void* dout, float* dq,
-                            float* dk, float* dv, float* d_offsets, void* workspace,
-                            size_t workspace_bytes, void* stream) {
+dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const void* k,
+                                  const void* v, const float* offsets, const float* lse,
+                                  const void* dout, float* dq, float* dk, float* dv,
+                                  float* d_offsets, void* workspace, size_t workspace_bytes,
+                                  void* stream, void* const* events) {
   dsa3d::Geometry g;
   uint64_t rows, io_bytes, f32_bytes, off_bytes;
   dsa3d_status st = check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes);
@@ -182,10 +183,18 @@ dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k
   }
   for (const Span& s : in)
     if (overlaps(sw, s)) return DSA3D_ERR_ALIAS;
-  const hipError_t e = dsa3d::launch_backward(g, desc->dtype == DSA3D_BF16, q, k, v, offsets, lse,
-                                              dout, dq, dk, dv, d_offsets, workspace,
-                                              static_cast<hipStream_t>(stream));
+  const hipError_t e = dsa3d::launch_backward(
+      g, desc->dtype == DSA3D_BF16, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace,
+      static_cast<hipStream_t>(stream), reinterpret_cast<hipEvent_t const*>(events));
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
+}
+
+dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
+                            const float* offsets, const float* lse, const void* dout, float* dq,
+                            float* dk, float* dv, float* d_offsets, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  return dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace,
+                              workspace_bytes, stream, nullptr);
 }
 
 }  // extern "C"

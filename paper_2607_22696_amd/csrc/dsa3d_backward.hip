@@ -562,7 +562,10 @@ int grid_for(int64_t items, int per_block = kBlockThreads, int cap = 1 << 20) {
 template <int D, bool BF16>
 hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const void* v,
                         const float* off, const float* lse, const void* dout, float* dq, float* dk,
-                        float* dv, float* doff, void* workspace, hipStream_t s) {
+                        float* dv, float* doff, void* workspace, hipStream_t s,
+                        hipEvent_t const* ev) {
+  // phase marks for the caller's timing events (none when ev is null)
+  auto mark = [&](int i) { return ev == nullptr ? hipSuccess : hipEventRecord(ev[i], s); };
   Workspace w = carve(g, workspace);
   const int64_t rows = (int64_t)g.B * g.N * g.heads;
   const int64_t cells = cells_per_bh(g) * g.B * g.heads;
@@ -578,6 +581,7 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   }
   const int tiles = tiles_for<D, BF16>(g);
   const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
+  if ((e = mark(0)) != hipSuccess) return e;
   {
     void* a[] = {(void*)&g,   (void*)&q,    (void*)&k,  (void*)&v,      (void*)&off,
                  (void*)&lse, (void*)&dout, (void*)&dq, (void*)&w.recs, (void*)&w.delta,
@@ -586,6 +590,7 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   }
+  if ((e = mark(1)) != hipSuccess) return e;
   {
     void* a[] = {(void*)&w.counts, (void*)&w.sums, (void*)&cells};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_reduce_kernel), dim3((unsigned)nsums),
@@ -602,6 +607,7 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
                         dim3(kScanThreads), c3, 0, s);
     if (e != hipSuccess) return e;
   }
+  if ((e = mark(2)) != hipSuccess) return e;
   {
     const int npoints = (int)points;
     void* a[] = {(void*)&g,        (void*)&off,   (void*)&w.recs, (void*)&w.delta,
@@ -610,6 +616,7 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   }
+  if ((e = mark(3)) != hipSuccess) return e;
   {
     using LY = Layout<D, BF16>;
     const int64_t vblocks = (int64_t)g.T * ((g.H + 1) / 2) * ((g.W + 1) / 2);
@@ -619,8 +626,9 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
                  (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&gtiles};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16>), dim3(gblocks),
                         dim3(kBlockThreads), a, 0, s);
+    if (e != hipSuccess) return e;
   }
-  return e;
+  return mark(4);
 }
 
 }  // namespace
@@ -630,9 +638,10 @@ size_t backward_workspace_bytes(const Geometry& g) { return carve(g, nullptr).by
 hipError_t launch_backward(const Geometry& g, bool bf16, const void* q, const void* k,
                            const void* v, const float* offsets, const float* lse, const void* dout,
                            float* dq, float* dk, float* dv, float* d_offsets, void* workspace,
-                           hipStream_t stream) {
+                           hipStream_t stream, hipEvent_t const* events) {
 #define DSA3D_BWD(DIM, BF) \
-  bwd_dispatch<DIM, BF>(g, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace, stream)
+  bwd_dispatch<DIM, BF>(g, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace, stream, \
+                         events)
   switch (g.D) {
     case 32:
       return bf16 ? DSA3D_BWD(32, true) : DSA3D_BWD(32, false);

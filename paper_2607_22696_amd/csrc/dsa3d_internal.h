@@ -32,6 +32,6 @@ size_t backward_workspace_bytes(const Geometry& g);
 hipError_t launch_backward(const Geometry& g, bool bf16, const void* q, const void* k,
                            const void* v, const float* offsets, const float* lse, const void* dout,
                            float* dq, float* dk, float* dv, float* d_offsets, void* workspace,
-                           hipStream_t stream);
+                           hipStream_t stream, hipEvent_t const* events);
 
 }  // namespace dsa3d

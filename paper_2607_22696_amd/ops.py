@@ -7,7 +7,8 @@ from __future__ import annotations
 
 import torch
 
-from ._binding import dsa3d_backward, dsa3d_backward_workspace_size, dsa3d_forward, make_desc
+from ._binding import (dsa3d_backward, dsa3d_backward_timed, dsa3d_backward_workspace_size,
+                       dsa3d_forward, make_desc)
 
 
 def _desc(q, kernel, scale):
@@ -44,9 +45,12 @@ def forward(q, k, v, offsets, kernel=(3, 3, 3), scale=0.0, need_lse=True, out=No
     return out, (lse if need_lse else None)
 
 
-def backward(q, k, v, offsets, lse, dout, kernel=(3, 3, 3), scale=0.0, grads=None, workspace=None):
+def backward(q, k, v, offsets, lse, dout, kernel=(3, 3, 3), scale=0.0, grads=None, workspace=None,
+             phase_events=None):
     """Returns (dq, dk, dv, d_offsets), all float32.  `workspace` (a uint8 CUDA tensor) is
-    allocated here when missing or too small."""
+    allocated here when missing or too small.  `phase_events`: optional list of
+    DSA3D_BACKWARD_PHASES + 1 created torch.cuda.Event objects marking the phases (see
+    dsa3d_backward_timed)."""
     desc = _desc(q, kernel, scale)
     if grads is None:
         f32 = dict(dtype=torch.float32, device=q.device)
@@ -56,5 +60,9 @@ def backward(q, k, v, offsets, lse, dout, kernel=(3, 3, 3), scale=0.0, grads=Non
     need = dsa3d_backward_workspace_size(desc)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
-    dsa3d_backward(desc, q, k, v, offsets, lse, dout, dq, dk, dv, doff, workspace, need)
+    if phase_events is None:
+        dsa3d_backward(desc, q, k, v, offsets, lse, dout, dq, dk, dv, doff, workspace, need)
+    else:
+        dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, doff, workspace, need,
+                             events=phase_events)
     return dq, dk, dv, doff

@@ -163,3 +163,36 @@ def test_backward_index_range_limit():
     d3 = good_desc(T=1 << 8, H=1 << 7, W=1 << 6, heads=2, kt=9, kh=9, kw=9)  # 2^22 rows, P=729
     assert dsa.dsa3d_backward_workspace_size(d3) == 0
     assert bwd(d3) == B.DSA3D_ERR_INVALID_SHAPE
+
+
+def bwd_timed(desc, events=None, **over):
+    names = ["q", "k", "v", "offsets", "lse", "dout", "dq", "dk", "dv", "d_offsets", "workspace"]
+    args = dict(zip(names, ptrs(len(names))))
+    args["workspace_bytes"] = 1 << 33
+    args.update(over)
+    return dsa.dsa3d_backward_timed(desc, *[args[n] for n in names[:-1]],
+                                    workspace=args["workspace"],
+                                    workspace_bytes=args["workspace_bytes"], stream=0,
+                                    events=events, check=False)
+
+
+def test_timed_backward_validates_like_backward():
+    d = good_desc()
+    need = dsa.dsa3d_backward_workspace_size(d)
+    names = ptrs(11)
+    cases = [dict(q=None), dict(d_offsets=None), dict(dq=ptrs(16)[15] + 4),
+             dict(workspace=None), dict(workspace_bytes=need - 1), dict(dk=names[6])]
+    fake_events = list(range(1 << 12, (1 << 12) + B.DSA3D_BACKWARD_PHASES + 1))
+    for over in cases:
+        want = bwd(d, **over)
+        assert want != B.DSA3D_OK
+        assert bwd_timed(d, **over) == want, over
+        # the events are only touched after every check has passed
+        assert bwd_timed(d, events=fake_events, **over) == want, over
+    bad = good_desc(kt=2)
+    assert bwd_timed(bad, events=fake_events) == B.DSA3D_ERR_INVALID_SHAPE
+
+
+def test_timed_backward_needs_one_event_per_phase_boundary():
+    with pytest.raises(ValueError):
+        bwd_timed(good_desc(), events=[1, 2, 3])

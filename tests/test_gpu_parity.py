@@ -182,7 +182,8 @@ def test_non_finite_and_huge_offsets_are_safe():
 
 
 def test_backward_repeatability():
-    """dk/dv use fp32 atomics: repeated runs may differ only by summation order."""
+    """dq and d_offsets are query-owned (bitwise repeatable); dk/dv sum each bin in the order
+    its points claimed their slots, so repeated runs may differ only by summation order."""
     w = small("repeat_bf16", T=4, H=8, W=8, heads=2, head_dim=64, dtype="bf16", seed=33,
               offsets=testgen.Dist(testgen.UNIFORM, -1.0, 1.0))
     q, k, v, off, _ = testgen.gen_inputs(w)
@@ -195,6 +196,30 @@ def test_backward_repeatability():
         assert np.array_equal(r[3], runs[0][3])  # d_offsets too
         for a in (1, 2):
             assert rel_err(r[a], runs[0][a]) < 1e-4
+
+
+def test_backward_timed_matches_untimed_and_marks_every_phase():
+    import paper_2607_22696_amd as dsa
+    w = small("timed_bf16", T=5, H=9, W=11, heads=2, head_dim=64, dtype="bf16", seed=34,
+              offsets=testgen.Dist(testgen.UNIFORM, -2.0, 2.0))
+    q, k, v, off, _ = testgen.gen_inputs(w)
+    dout = testgen.gen_tensor(w, testgen.TID_DOUT, w.qkv_shape(), w.dout, True)
+    qd, kd, vd, od, out, lse = run_forward(w, q, k, v, off)
+    gd = to_device(dout, True)
+    kern = (w.kt, w.kh, w.kw)
+    plain = [to_host(t) for t in dsa.backward(qd, kd, vd, od, lse, gd, kernel=kern)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(dsa.DSA3D_BACKWARD_PHASES + 1)]
+    for e in evs:  # creates the underlying HIP events
+        e.record()
+    timed = dsa.backward(qd, kd, vd, od, lse, gd, kernel=kern, phase_events=evs)
+    torch.cuda.synchronize()
+    timed = [to_host(t) for t in timed]
+    assert np.array_equal(timed[0], plain[0]) and np.array_equal(timed[3], plain[3])
+    for a in (1, 2):
+        assert rel_err(timed[a], plain[a]) < 1e-4
+    ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(dsa.DSA3D_BACKWARD_PHASES)]
+    say(f"  phase ms {ms}")
+    assert all(t > 0.0 for t in ms)
 
 
 # ----------------------------------------------------------------------------- full size
