@@ -239,15 +239,17 @@ def main():
     w = testgen.WORKLOADS[args.workload]
     do_bwd = w.backward and not args.forward_only
     t_gen = time.perf_counter()
-    host = testgen.gen_inputs(w)
+    host = testgen.gen_inputs(w, progress=lambda m: print(m, file=sys.stderr, flush=True))
     if host[4] is None and do_bwd:
         host = host[:4] + (testgen.gen_tensor(w, testgen.TID_DOUT, w.qkv_shape(), w.dout, True),)
     q, k, v, off, dout = host
     bf = w.dtype == "bf16"
+    print("copying inputs to the GPU", file=sys.stderr, flush=True)
     qd, kd, vd = (to_device(a, bf) for a in (q, k, v))
     od = to_device(off, False)
     gd = to_device(dout, bf) if do_bwd else None
     t_gen = time.perf_counter() - t_gen
+    print(f"inputs resident after {t_gen:.1f} s; timing", file=sys.stderr, flush=True)
     kern = (w.kt, w.kh, w.kw)
     out, lse = dsa.forward(qd, kd, vd, od, kernel=kern)
     grads = None

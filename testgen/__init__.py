@@ -163,6 +163,14 @@ WORKLOADS = {
     # forward + backward, 3x5x5 kernel (75 points), offsets uniform in [-8, 8].
     "wide_64x68x120_p75": Workload("wide_64x68x120_p75", 1, 64, 68, 120, 24, 128, 3, 5, 5, "bf16",
                                    N01, Dist(UNIFORM, -8.0, 8.0), seed=4, backward=True),
+    # The paper's kernel, 3x7x7 (147 points), forward + backward on the 64-frame 1080p grid.
+    "paper_3x7x7_64x68x120": Workload("paper_3x7x7_64x68x120", 1, 64, 68, 120, 24, 128, 3, 7, 7,
+                                      "bf16", N01, Dist(NORMAL, 0.0, 1.0, -3.0, 3.0), seed=5,
+                                      backward=True),
+    # The paper's kernel on 256 frames of 1080p (2,088,960 tokens), forward.
+    "paper_3x7x7_1080p_256f": Workload("paper_3x7x7_1080p_256f", 1, 256, 68, 120, 24, 128, 3, 7,
+                                       7, "bf16", N01, Dist(NORMAL, 0.0, 1.0, -3.0, 3.0), seed=6,
+                                       backward=False),
 }
 
 
@@ -171,11 +179,17 @@ def gen_tensor(w: Workload, tid: int, shape, dist: Dist, io: bool, start: int = 
     return fill(out, w.seed, tid, start, dist)
 
 
-def gen_inputs(w: Workload):
-    """Full host copies of q, k, v (io dtype), offsets (fp32) and dout (io dtype)."""
-    q = gen_tensor(w, TID_Q, w.qkv_shape(), w.qkv, True)
-    k = gen_tensor(w, TID_K, w.qkv_shape(), w.qkv, True)
-    v = gen_tensor(w, TID_V, w.qkv_shape(), w.qkv, True)
-    off = gen_tensor(w, TID_OFF, w.off_shape(), w.offsets, False)
-    dout = gen_tensor(w, TID_DOUT, w.qkv_shape(), w.dout, True) if w.backward else None
+def gen_inputs(w: Workload, progress=None):
+    """Full host copies of q, k, v (io dtype), offsets (fp32) and dout (io dtype).
+    `progress`, if given, is called with a short message before each tensor."""
+    def one(name, tid, shape, dist, io):
+        if progress is not None:
+            progress(f"generating {name} {shape} of {w.name}")
+        return gen_tensor(w, tid, shape, dist, io)
+
+    q = one("q", TID_Q, w.qkv_shape(), w.qkv, True)
+    k = one("k", TID_K, w.qkv_shape(), w.qkv, True)
+    v = one("v", TID_V, w.qkv_shape(), w.qkv, True)
+    off = one("offsets", TID_OFF, w.off_shape(), w.offsets, False)
+    dout = one("dout", TID_DOUT, w.qkv_shape(), w.dout, True) if w.backward else None
     return q, k, v, off, dout

@@ -233,7 +233,7 @@ def sampled_rows(w, n, rng):
 
 def full_size_forward(w, nsamp):
     say(f"full-size {w.name}: generating {w.queries} rows ...")
-    q, k, v, off, dout = testgen.gen_inputs(w)
+    q, k, v, off, dout = testgen.gen_inputs(w, progress=say)
     say("  forward on GPU ...")
     qd, kd, vd, od, out, lse = run_forward(w, q, k, v, off)
     rng = np.random.default_rng(w.seed)
@@ -309,3 +309,12 @@ def test_wide_64x68x120_p75_full_size():
     w = testgen.WORKLOADS["wide_64x68x120_p75"]
     host, dev, out, lse, rows = full_size_forward(w, 4096)
     full_size_backward(w, host, dev, out, lse, rows, slab_frames=[0, 37], slab_heads=[5])
+
+
+@pytest.mark.slow
+def test_paper_3x7x7_64x68x120_full_size():
+    """The paper's 3x7x7 kernel (147 points) on the 64-frame 1080p grid, forward and
+    backward at full size; sampled rows plus dK/dV frame slabs are checked."""
+    w = testgen.WORKLOADS["paper_3x7x7_64x68x120"]
+    host, dev, out, lse, rows = full_size_forward(w, 2048)
+    full_size_backward(w, host, dev, out, lse, rows, slab_frames=[0, 40], slab_heads=[11])
