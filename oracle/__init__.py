@@ -2,9 +2,10 @@
 
 TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
 bench's CPU-baseline leg may import this package.  It wraps ``dsa3d_oracle.c``
-(plain C, fp64 accumulation, OpenMP) with ctypes and shares nothing with the
-GPU library.  The arithmetic and the readings it follows are described at the
-top of ``dsa3d_oracle.c``.
+(the attention term) and ``dwconv3d_oracle.c`` (the depthwise 3D convolution term
+and the offset network's depthwise convolution), plain C with fp64 accumulation and
+OpenMP, with ctypes, and shares nothing with the GPU library.  The arithmetic and
+the readings it follows are described at the top of each C file.
 """
 from __future__ import annotations
 
@@ -16,7 +17,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "dsa3d_oracle.c")
+_SRCS = [os.path.join(_HERE, "dsa3d_oracle.c"), os.path.join(_HERE, "dwconv3d_oracle.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 
@@ -24,7 +25,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11",
-                               _SRC, "-o", tmp, "-lm"])
+                               *_SRCS, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -34,6 +35,13 @@ class _Problem(ctypes.Structure):
                 ("W", ctypes.c_int64), ("heads", ctypes.c_int64), ("D", ctypes.c_int64),
                 ("kt", ctypes.c_int64), ("kh", ctypes.c_int64), ("kw", ctypes.c_int64),
                 ("scale", ctypes.c_double), ("bf16", ctypes.c_int32), ("pad_", ctypes.c_int32)]
+
+
+class _Conv(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int64), ("T", ctypes.c_int64), ("H", ctypes.c_int64),
+                ("W", ctypes.c_int64), ("C", ctypes.c_int64), ("kt", ctypes.c_int64),
+                ("kh", ctypes.c_int64), ("kw", ctypes.c_int64), ("bf16", ctypes.c_int32),
+                ("pad_", ctypes.c_int32)]
 
 
 _lib = None
@@ -54,6 +62,12 @@ def _load():
         lib.orc_backward_rows.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, vp, vp,
                                           ctypes.c_int64, vp, vp]
         lib.orc_backward_rows.restype = ctypes.c_int
+        lib.orc_dwconv_forward.argtypes = [ctypes.POINTER(_Conv), vp, vp, vp, ctypes.c_int64,
+                                           ctypes.c_int64, vp]
+        lib.orc_dwconv_forward.restype = ctypes.c_int
+        lib.orc_dwconv_backward.argtypes = [ctypes.POINTER(_Conv), vp, vp, vp, ctypes.c_int64,
+                                            ctypes.c_int64, vp, vp, vp]
+        lib.orc_dwconv_backward.restype = ctypes.c_int
         lib.orc_max_threads.argtypes = []
         lib.orc_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -168,3 +182,52 @@ def backward(shape, dtype, q, k, v, off, dout, scale=None):
             dk[b, :, :, :, m] = kk
             dv[b, :, :, :, m] = vv
     return dq, dk, dv, doff
+
+
+# ----------------------------------------------------------------------------- depthwise conv
+
+def _conv(shape, dtype):
+    B, T, H, W, C, kt, kh, kw = shape
+    return _Conv(B, T, H, W, C, kt, kh, kw, 1 if dtype == "bf16" else 0, 0)
+
+
+def dwconv_forward(shape, dtype, x, w, bias=None, frames=None):
+    """Depthwise 3D convolution y = conv(x) + bias of frames [t0, t1) (all if None).
+
+    shape = (B, T, H, W, C, kt, kh, kw); x is [B,T,H,W,C] (float32, or uint16 bf16 bit
+    patterns when dtype == "bf16"); w is float32 [C,kt,kh,kw]; bias float32 [C] or None.
+    Returns y[B, t1-t0, H, W, C] in fp64."""
+    pr = _conv(shape, dtype)
+    x = _check_io(x, dtype)
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    bias = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    B, T, H, W, C = shape[:5]
+    t0, t1 = (0, T) if frames is None else frames
+    y = np.empty((B, t1 - t0, H, W, C), dtype=np.float64)
+    rc = _load().orc_dwconv_forward(ctypes.byref(pr), x.ctypes.data, w.ctypes.data,
+                                    None if bias is None else bias.ctypes.data, t0, t1,
+                                    y.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle dwconv forward: malformed problem")
+    return y
+
+
+def dwconv_backward(shape, dtype, x, w, dy, frames=None, weight_grads=True):
+    """(dx[B, t1-t0, H, W, C], dw[C,kt,kh,kw], dbias[C]) in fp64; dx covers frames [t0, t1)
+    (all if None); dw and dbias (None unless weight_grads) sum over the whole grid."""
+    pr = _conv(shape, dtype)
+    x, dy = _check_io(x, dtype), _check_io(dy, dtype)
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    B, T, H, W, C, kt, kh, kw = shape
+    t0, t1 = (0, T) if frames is None else frames
+    dx = np.empty((B, t1 - t0, H, W, C), dtype=np.float64)
+    dw = np.empty((C, kt, kh, kw), dtype=np.float64) if weight_grads else None
+    db = np.empty(C, dtype=np.float64) if weight_grads else None
+    rc = _load().orc_dwconv_backward(ctypes.byref(pr), x.ctypes.data, w.ctypes.data,
+                                     dy.ctypes.data, t0, t1, dx.ctypes.data,
+                                     None if dw is None else dw.ctypes.data,
+                                     None if db is None else db.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle dwconv backward: malformed problem")
+    return dx, dw, db
+
