@@ -28,18 +28,31 @@ METRIC = "3D-DSA fwd+bwd queries/s and achieved HBM GB/s (% of peak) at 1 GPU"
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 VALU_PEAK_TFLOPS = 157.3        # MI355X fp32 vector peak (2 FLOP/lane/clk: dot2 / dual issue)
 DEFAULT_WORKLOAD = "fwdbwd_64x34x60"
+DEFAULT_CONV_WORKLOAD = "dwconv_1080p_256f"
+CONV_METRIC = "DWConv3D fwd+bwd tokens/s and achieved HBM GB/s (% of peak) at 1 GPU"
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2607_22696_amd", "csrc")
 
 
-def kernel_source_hash() -> str:
-    """Hash of the HIP sources: counter figures taken from other sources are stale."""
+# Device sources of each kernel family: counter figures taken from other sources are stale.
+FAMILY_SOURCES = {
+    "dsa": ["dsa3d_device.h", "dsa3d_forward.hip", "dsa3d_backward.hip"],
+    "dwconv": ["dsa3d_device.h", "dwconv3d.hip"],
+}
+
+
+def kernel_source_hash(family: str = "dsa") -> str:
+    """Hash of the device sources of one kernel family."""
     import hashlib
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
+    for name in FAMILY_SOURCES[family]:
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
+
+
+def workload_family(workload: str) -> str:
+    return "dwconv" if workload.startswith("dwconv") else "dsa"
 
 
 def kernel_base(name: str) -> str:
@@ -69,7 +82,7 @@ def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
     cw = per_kernel(copyw_dir)["__amd_rocclr_copyBuffer"]
     fetch_scale = (sum(cf) / len(cf)) / true_bytes   # counter bytes per byte actually read
     write_scale = (sum(cw) / len(cw)) / true_bytes
-    out = {"workload": workload, "kernel_source_hash": kernel_source_hash(),
+    out = {"workload": workload, "kernel_source_hash": kernel_source_hash(workload_family(workload)),
            "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
            "kernels": {}}
     for k in fetch:
@@ -94,7 +107,7 @@ def measured_traffic(workload, kernel):
         return None
     with open(path) as fh:
         d = json.load(fh)
-    if d.get("kernel_source_hash") != kernel_source_hash():
+    if d.get("kernel_source_hash") != kernel_source_hash(workload_family(workload)):
         return None
     k = d.get("kernels", {}).get(kernel)
     return None if k is None else k["hbm_bytes"]
@@ -185,12 +198,120 @@ def cpu_baseline(w, host, budget_s, backward=True):
                       f"scaled to query tokens (all {w.heads} heads)"}
 
 
+def conv_algorithmic(w):
+    """Algorithmic HBM bytes and FLOPs per launch of the depthwise-conv kernels, per element
+    (token, channel), s = bytes per x / y / dy element, taps = kt kh kw:
+      dwconv_kernel (forward)   x read, y written: 2 s;         2 taps FLOPs
+      dwconv_kernel (dx)        dy read, dx (fp32) written: s + 4; 2 taps FLOPs
+      dwconv_wgrad_kernel       x and dy read: 2 s;              2 taps FLOPs
+    (the filter, the bias and the per-slice partial sums are a few MB)."""
+    s = 2 if w.dtype == "bf16" else 4
+    n = w.tokens * w.C
+    f = 2 * w.taps * n
+    return {"dwconv_forward": {"bytes": n * 2 * s, "flops": f},
+            "dwconv_dx": {"bytes": n * (s + 4), "flops": f},
+            "dwconv_wgrad": {"bytes": n * 2 * s, "flops": f}}
+
+
+def conv_cpu_baseline(w, host, budget_s):
+    """The conv oracle (forward and dx of one frame at a time, fp64) for about budget_s
+    seconds; tokens per second."""
+    import oracle
+    x, dy, wt, bias = host
+    frames = 0
+    t0 = time.perf_counter()
+    while frames < w.T and time.perf_counter() - t0 < budget_s:
+        oracle.dwconv_forward(w.shape8(), w.dtype, x, wt, bias, frames=(frames, frames + 1))
+        oracle.dwconv_backward(w.shape8(), w.dtype, x, wt, dy, frames=(frames, frames + 1),
+                               weight_grads=False)
+        frames += 1
+    dt = time.perf_counter() - t0
+    toks = frames * w.H * w.W * w.B
+    return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"frames [0,{frames}) of {w.name}: {toks} tokens x {w.C} channels, forward "
+                      f"+ dx (no weight gradient), fp64, {dt:.1f} s"}
+
+
+def bench_dwconv(args, torch, dsa, testgen, to_device):
+    """One step = forward, dx, and the weight and bias gradients of the depthwise conv."""
+    w = testgen.CONV_WORKLOADS[args.workload]
+    t_gen = time.perf_counter()
+    host = testgen.gen_conv_inputs(w, progress=lambda m: print(m, file=sys.stderr, flush=True))
+    x, dy, wt, bias = host
+    bf = w.dtype == "bf16"
+    xd, dyd = to_device(x, bf), to_device(dy, bf)
+    wd, bd = to_device(wt, False), to_device(bias, False)
+    t_gen = time.perf_counter() - t_gen
+    y = torch.empty_like(xd)
+    dx = torch.empty(xd.shape, dtype=torch.float32, device=xd.device)
+    desc = dsa.make_conv_desc(w.B, w.T, w.H, w.W, w.C, w.kt, w.kh, w.kw, w.dtype)
+    ws = torch.empty(dsa.dsa3d_dwconv3d_backward_workspace_size(desc), dtype=torch.uint8,
+                     device=xd.device)
+    dwt = torch.empty(wt.shape, dtype=torch.float32, device=xd.device)
+    dbt = torch.empty(bias.shape, dtype=torch.float32, device=xd.device)
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+
+    def step(s=None):
+        if s is not None:
+            ev[s][0].record()
+        dsa.dwconv3d_forward(xd, wd, bd, out=y)
+        if s is not None:
+            ev[s][1].record()
+        dsa.dwconv3d_backward(xd, wd, dyd, need_dweight=False, need_dbias=False, dx=dx)
+        if s is not None:
+            ev[s][2].record()
+        dsa.dsa3d_dwconv3d_backward(desc, xd, wd, dyd, None, dwt, dbt, ws, ws.numel())
+        if s is not None:
+            ev[s][3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for s in range(K):
+        step(s)
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / K
+    kernel_ms = {n: sum(e[i].elapsed_time(e[i + 1]) for e in ev) / K
+                 for i, n in enumerate(["dwconv_forward", "dwconv_dx", "dwconv_wgrad"])}
+    alg = conv_algorithmic(w)
+    kname = max(kernel_ms, key=lambda n: kernel_ms[n])
+    roof = roofline(alg[kname], kernel_ms[kname])
+    roof["traffic"] = None
+    roof["kernel"] = kname
+    roof["avg_launch_ms"] = round(kernel_ms[kname], 4)
+    step_bytes = sum(a["bytes"] for a in alg.values())
+    res = {
+        "metric": CONV_METRIC, "value": round(w.tokens / (ms_step * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded Philox inputs shaped like the paper's video-latent grids)",
+        "config": {"workload": w.name, "grid_TxHxW": [w.T, w.H, w.W], "batch": w.B,
+                   "channels": w.C, "kernel": [w.kt, w.kh, w.kw], "parallelism": "single GPU"},
+        "kernel_ms": {n: round(t, 4) for n, t in kernel_ms.items()},
+        "kernel_roofline": {n: roofline(alg[n], t) for n, t in kernel_ms.items()},
+        "hbm_gbs_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": roof, "input_gen_s": round(t_gen, 1),
+    }
+    if args.cpu_budget > 0:
+        res["cpu_baseline"] = conv_cpu_baseline(w, host, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--op", choices=["dsa", "dwconv"], default="dsa",
+                    help="dsa: the 3D-DSA operator (default); dwconv: the depthwise 3D "
+                         "convolution term of Eq. (1) (workloads dwconv_*)")
+    ap.add_argument("--workload", default=None,
+                    help=f"default {DEFAULT_WORKLOAD} (dsa) or {DEFAULT_CONV_WORKLOAD} (dwconv)")
     ap.add_argument("--forward-only", action="store_true",
                     help="time the forward alone (workloads without a backward pass)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
@@ -203,6 +324,8 @@ def main():
                          "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
     args = ap.parse_args()
 
+    if args.workload is None:
+        args.workload = DEFAULT_CONV_WORKLOAD if args.op == "dwconv" else DEFAULT_WORKLOAD
     if args.pmc_summary:
         pmc_summary(args.workload, *args.pmc_summary, copy_mib=args.copy_probe or 1024)
         return
@@ -236,6 +359,9 @@ def main():
                           "gbs_read_plus_write": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}))
         return
     dsa.load()
+    if args.op == "dwconv":
+        bench_dwconv(args, torch, dsa, testgen, to_device)
+        return
     w = testgen.WORKLOADS[args.workload]
     do_bwd = w.backward and not args.forward_only
     t_gen = time.perf_counter()

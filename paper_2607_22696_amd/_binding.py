@@ -28,8 +28,12 @@ DSA3D_MAX_POINTS = 1024
 
 DSA3D_BACKWARD_PHASES = 4
 
+DSA3D_DWCONV_MAX_TAPS = 128
+
 EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_timed",
-            "dsa3d_backward_workspace_size", "dsa3d_status_string", "dsa3d_abi_version")
+            "dsa3d_backward_workspace_size", "dsa3d_status_string", "dsa3d_abi_version",
+            "dsa3d_dwconv3d_forward", "dsa3d_dwconv3d_backward_workspace_size",
+            "dsa3d_dwconv3d_backward")
 
 
 class dsa3d_desc(ctypes.Structure):
@@ -37,6 +41,12 @@ class dsa3d_desc(ctypes.Structure):
                 ("width", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("kt", ctypes.c_int32), ("kh", ctypes.c_int32), ("kw", ctypes.c_int32),
                 ("scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class dsa3d_dwconv_desc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("frames", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("channels", ctypes.c_int32), ("kt", ctypes.c_int32),
+                ("kh", ctypes.c_int32), ("kw", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
 class Dsa3dError(RuntimeError):
@@ -65,6 +75,14 @@ def load():
         lib.dsa3d_backward_timed.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                              ctypes.c_size_t, vp, ctypes.POINTER(vp)]
         lib.dsa3d_backward_timed.restype = ctypes.c_int
+        cd = ctypes.POINTER(dsa3d_dwconv_desc)
+        lib.dsa3d_dwconv3d_forward.argtypes = [cd, vp, vp, vp, vp, ctypes.c_int, vp]
+        lib.dsa3d_dwconv3d_forward.restype = ctypes.c_int
+        lib.dsa3d_dwconv3d_backward_workspace_size.argtypes = [cd]
+        lib.dsa3d_dwconv3d_backward_workspace_size.restype = ctypes.c_size_t
+        lib.dsa3d_dwconv3d_backward.argtypes = [cd, vp, vp, vp, vp, ctypes.c_int, vp, vp, vp,
+                                                ctypes.c_size_t, vp]
+        lib.dsa3d_dwconv3d_backward.restype = ctypes.c_int
         lib.dsa3d_backward_workspace_size.argtypes = [pd]
         lib.dsa3d_backward_workspace_size.restype = ctypes.c_size_t
         lib.dsa3d_status_string.argtypes = [ctypes.c_int]
@@ -146,6 +164,37 @@ def dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offset
                                      _ptr(workspace), workspace_bytes, _stream(stream), arr)
     if check and st != DSA3D_OK:
         raise Dsa3dError(st, "dsa3d_backward_timed")
+    return st
+
+
+def make_conv_desc(B, T, H, W, C, kt, kh, kw, dtype="bf16") -> dsa3d_dwconv_desc:
+    return dsa3d_dwconv_desc(B, T, H, W, C, kt, kh, kw,
+                             DSA3D_BF16 if dtype == "bf16" else DSA3D_F32)
+
+
+def dsa3d_dwconv3d_forward(desc, x, weight, bias, y, accumulate=False, stream=None,
+                           check=True) -> int:
+    st = load().dsa3d_dwconv3d_forward(ctypes.byref(desc) if desc is not None else None, _ptr(x),
+                                       _ptr(weight), _ptr(bias), _ptr(y), int(bool(accumulate)),
+                                       _stream(stream))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_dwconv3d_forward")
+    return st
+
+
+def dsa3d_dwconv3d_backward_workspace_size(desc) -> int:
+    return load().dsa3d_dwconv3d_backward_workspace_size(ctypes.byref(desc))
+
+
+def dsa3d_dwconv3d_backward(desc, x, weight, dy, dx, dweight, dbias, workspace=None,
+                            workspace_bytes=0, accumulate_dx=False, stream=None,
+                            check=True) -> int:
+    st = load().dsa3d_dwconv3d_backward(ctypes.byref(desc) if desc is not None else None, _ptr(x),
+                                        _ptr(weight), _ptr(dy), _ptr(dx),
+                                        int(bool(accumulate_dx)), _ptr(dweight), _ptr(dbias),
+                                        _ptr(workspace), workspace_bytes, _stream(stream))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_dwconv3d_backward")
     return st
 
 

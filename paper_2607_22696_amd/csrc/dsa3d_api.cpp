@@ -7,22 +7,15 @@
 #include <cmath>
 #include <cstdint>
 
+#include "api_util.h"
 #include "dsa3d_internal.h"
 
 namespace {
 
-struct Span {
-  uintptr_t lo, hi;  // [lo, hi)
-};
-
-bool overlaps(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
-
-bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
-
-Span span_of(const void* p, uint64_t bytes) {
-  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
-  return Span{lo, lo + bytes};
-}
+using dsa3d::api::aligned;
+using dsa3d::api::overlaps;
+using dsa3d::api::Span;
+using dsa3d::api::span_of;
 
 // Checks the descriptor and fills the kernel geometry and the tensor sizes.
 dsa3d_status check_desc(const dsa3d_desc* d, dsa3d::Geometry* g, uint64_t* rows, uint64_t* io_bytes,

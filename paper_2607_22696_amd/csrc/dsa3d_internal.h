@@ -34,4 +34,26 @@ hipError_t launch_backward(const Geometry& g, bool bf16, const void* q, const vo
                            float* dq, float* dk, float* dv, float* d_offsets, void* workspace,
                            hipStream_t stream, hipEvent_t const* events);
 
+// ---------------------------------------------------------------------------- depthwise conv
+
+// Depthwise 3D convolution geometry (validated on the host; filled by conv_plan).
+struct ConvGeometry {
+  int B, T, H, W, C;         // batch, frames, height, width, channels
+  int bf16;                  // storage of x, y and dy (set before conv_plan)
+  int stream;                // the time-streaming kernels apply (set by conv_plan)
+  int kt, kh, kw, taps;      // odd filter size and its tap count
+  int chunks;                // 128-channel chunks
+  int strips, sg, hq;        // 8-token strips along x, strips per brick, 4-row quads along y
+  int tiles_per_bc;          // tiles per (channel chunk, batch item), brick padding included
+  int wg_blocks;             // weight-gradient blocks per (channel chunk, filter plane)
+};
+
+void conv_plan(ConvGeometry& g);
+size_t conv_workspace_bytes(const ConvGeometry& g);
+hipError_t launch_conv_forward(const ConvGeometry& g, bool bf16, const void* x, const float* w,
+                               const float* bias, void* y, int accumulate, hipStream_t stream);
+hipError_t launch_conv_backward(const ConvGeometry& g, bool bf16, const void* x, const float* w,
+                                const void* dy, float* dx, int accumulate_dx, float* dw, float* db,
+                                void* workspace, hipStream_t stream);
+
 }  // namespace dsa3d

@@ -8,7 +8,8 @@ from __future__ import annotations
 import torch
 
 from ._binding import (dsa3d_backward, dsa3d_backward_timed, dsa3d_backward_workspace_size,
-                       dsa3d_forward, make_desc)
+                       dsa3d_dwconv3d_backward, dsa3d_dwconv3d_backward_workspace_size,
+                       dsa3d_dwconv3d_forward, dsa3d_forward, make_conv_desc, make_desc)
 
 
 def _desc(q, kernel, scale):
@@ -66,3 +67,49 @@ def backward(q, k, v, offsets, lse, dout, kernel=(3, 3, 3), scale=0.0, grads=Non
         dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, doff, workspace, need,
                              events=phase_events)
     return dq, dk, dv, doff
+
+
+def _conv_desc(x, weight):
+    if x.dim() != 5:
+        raise ValueError("x must be [B, T, H, W, C]")
+    B, T, H, W, C = x.shape
+    if weight.dim() != 4 or weight.shape[0] != C:
+        raise ValueError("weight must be [C, kt, kh, kw]")
+    kt, kh, kw = weight.shape[1:]
+    return make_conv_desc(B, T, H, W, C, kt, kh, kw,
+                          "bf16" if x.dtype == torch.bfloat16 else "f32")
+
+
+def dwconv3d_forward(x, weight, bias=None, out=None, accumulate=False):
+    """Depthwise 3D convolution (the DWConv3D term of Eq. (1)): x [B,T,H,W,C] (bf16 or fp32),
+    weight float32 [C,kt,kh,kw], bias float32 [C] or None.  Returns out (x's dtype); with
+    accumulate=True the result is added to `out`."""
+    desc = _conv_desc(x, weight)
+    if out is None:
+        if accumulate:
+            raise ValueError("accumulate needs an output to add to")
+        out = torch.empty_like(x)
+    dsa3d_dwconv3d_forward(desc, x, weight, bias, out, accumulate)
+    return out
+
+
+def dwconv3d_backward(x, weight, dy, need_dx=True, need_dweight=True, need_dbias=True,
+                      dx=None, accumulate_dx=False, workspace=None):
+    """Returns (dx, dweight, dbias) as float32 (None where not requested)."""
+    desc = _conv_desc(x, weight)
+    f32 = dict(dtype=torch.float32, device=x.device)
+    if need_dx and dx is None:
+        if accumulate_dx:
+            raise ValueError("accumulate_dx needs a dx to add to")
+        dx = torch.empty(x.shape, **f32)
+    dx = dx if need_dx else None
+    dw = torch.empty(weight.shape, **f32) if need_dweight else None
+    db = torch.empty(weight.shape[0], **f32) if need_dbias else None
+    need = 0
+    if dw is not None or db is not None:
+        need = dsa3d_dwconv3d_backward_workspace_size(desc)
+        if workspace is None or workspace.numel() < need:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    dsa3d_dwconv3d_backward(desc, x, weight, dy, dx, dw, db, workspace, need, accumulate_dx)
+    return dx, dw, db
+

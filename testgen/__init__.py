@@ -193,3 +193,71 @@ def gen_inputs(w: Workload, progress=None):
     off = one("offsets", TID_OFF, w.off_shape(), w.offsets, False)
     dout = one("dout", TID_DOUT, w.qkv_shape(), w.dout, True) if w.backward else None
     return q, k, v, off, dout
+
+
+# ----------------------------------------------------------------------------- depthwise conv
+
+TID_CONV_X, TID_CONV_DY, TID_CONV_W, TID_CONV_B = 10, 11, 12, 13
+
+
+@dataclasses.dataclass(frozen=True)
+class ConvWorkload:
+    """A synthetic depthwise 3D convolution problem: x and dy ~ N(0, 1) on a T x H x W grid of
+    C channels, weights N(0, 1/taps) (the scale of a fan-in initialisation), bias N(0, 0.1)."""
+    name: str
+    B: int
+    T: int
+    H: int
+    W: int
+    C: int
+    kt: int
+    kh: int
+    kw: int
+    dtype: str
+    seed: int
+
+    @property
+    def taps(self):
+        return self.kt * self.kh * self.kw
+
+    @property
+    def tokens(self):
+        return self.B * self.T * self.H * self.W
+
+    def shape8(self):
+        return (self.B, self.T, self.H, self.W, self.C, self.kt, self.kh, self.kw)
+
+    def x_shape(self):
+        return (self.B, self.T, self.H, self.W, self.C)
+
+    def np_io_dtype(self):
+        return np.float32 if self.dtype == "f32" else np.uint16
+
+    def with_grid(self, **kw) -> "ConvWorkload":
+        return dataclasses.replace(self, **kw)
+
+
+def gen_conv_inputs(w: ConvWorkload, progress=None):
+    """Host copies of x, dy (io dtype), weight [C,kt,kh,kw] and bias [C] (float32)."""
+    def one(name, tid, shape, dist, io):
+        if progress is not None:
+            progress(f"generating {name} {shape} of {w.name}")
+        out = np.empty(shape, dtype=w.np_io_dtype() if io else np.float32)
+        return fill(out, w.seed, tid, 0, dist)
+
+    x = one("x", TID_CONV_X, w.x_shape(), N01, True)
+    dy = one("dy", TID_CONV_DY, w.x_shape(), N01, True)
+    wt = one("weight", TID_CONV_W, (w.C, w.kt, w.kh, w.kw), Dist(NORMAL, 0.0, w.taps ** -0.5),
+             False)
+    bias = one("bias", TID_CONV_B, (w.C,), Dist(NORMAL, 0.0, 0.1), False)
+    return x, dy, wt, bias
+
+
+CONV_WORKLOADS = {
+    # The DWConv3D term on 256 frames of 1080p: 2,088,960 tokens x 3072 channels (24 x 128).
+    "dwconv_1080p_256f": ConvWorkload("dwconv_1080p_256f", 1, 256, 68, 120, 3072, 3, 3, 3, "bf16",
+                                      seed=20),
+    # The same term on the forward + backward grid: 130,560 tokens x 1024 channels (16 x 64).
+    "dwconv_64x34x60": ConvWorkload("dwconv_64x34x60", 1, 64, 34, 60, 1024, 3, 3, 3, "bf16",
+                                    seed=21),
+}

@@ -10,14 +10,17 @@ import pytest
 import paper_2607_22696_amd as dsa
 from paper_2607_22696_amd import _binding as B
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
-                      "dsa3d.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
 
 
 def declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(dsa3d_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in sorted(os.listdir(INCLUDE)):
+        if h.endswith(".h"):
+            src = open(os.path.join(INCLUDE, h)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(dsa3d_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function():
@@ -196,3 +199,106 @@ def test_timed_backward_validates_like_backward():
 def test_timed_backward_needs_one_event_per_phase_boundary():
     with pytest.raises(ValueError):
         bwd_timed(good_desc(), events=[1, 2, 3])
+
+
+# ----------------------------------------------------------------------------- depthwise conv
+
+def good_conv(**kw):
+    d = dict(B=1, T=4, H=5, W=6, C=8, kt=3, kh=3, kw=3, dtype="f32")
+    d.update(kw)
+    return dsa.make_conv_desc(d["B"], d["T"], d["H"], d["W"], d["C"], d["kt"], d["kh"], d["kw"],
+                              d["dtype"])
+
+
+def conv_fwd(desc, **over):
+    x, w, b, y = ptrs(4)
+    args = dict(x=x, weight=w, bias=b, y=y)
+    args.update(over)
+    return dsa.dsa3d_dwconv3d_forward(desc, args["x"], args["weight"], args["bias"], args["y"],
+                                      stream=0, check=False)
+
+
+def conv_bwd(desc, **over):
+    names = ["x", "weight", "dy", "dx", "dweight", "dbias", "workspace"]
+    args = dict(zip(names, ptrs(len(names))))
+    args["workspace_bytes"] = 1 << 33
+    args.update(over)
+    return dsa.dsa3d_dwconv3d_backward(desc, args["x"], args["weight"], args["dy"], args["dx"],
+                                       args["dweight"], args["dbias"], args["workspace"],
+                                       args["workspace_bytes"], stream=0, check=False)
+
+
+def test_conv_desc_layout_matches_header():
+    assert ctypes.sizeof(B.dsa3d_dwconv_desc) == 9 * 4
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=0), B.DSA3D_ERR_INVALID_SHAPE), (dict(C=0), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(C=7), B.DSA3D_ERR_INVALID_SHAPE), (dict(kt=2), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(kw=4), B.DSA3D_ERR_INVALID_SHAPE), (dict(kh=9), B.DSA3D_ERR_UNSUPPORTED),
+    (dict(kt=3, kh=7, kw=7), B.DSA3D_ERR_UNSUPPORTED),          # 147 taps
+    (dict(kt=9, kh=3, kw=3), B.DSA3D_OK),                       # 81 taps, kt free
+    (dict(B=1 << 16, T=1 << 8, H=1 << 4, W=1 << 3), B.DSA3D_ERR_INVALID_SHAPE),  # 2^31 tokens
+])
+def test_conv_descriptor_errors(kw, status):
+    assert conv_fwd(good_conv(**kw), x=None if status == B.DSA3D_OK else ptrs(1)[0]) == (
+        B.DSA3D_ERR_NULL_POINTER if status == B.DSA3D_OK else status)
+
+
+def test_conv_bad_dtype_and_null_pointers():
+    d = good_conv()
+    d.dtype = 5
+    assert conv_fwd(d) == B.DSA3D_ERR_UNSUPPORTED
+    assert dsa.dsa3d_dwconv3d_forward(None, *ptrs(4), stream=0, check=False) == \
+        B.DSA3D_ERR_NULL_POINTER
+    d = good_conv()
+    for name in ["x", "weight", "y"]:
+        assert conv_fwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+    for name in ["x", "weight", "dy"]:
+        assert conv_bwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+    assert conv_bwd(d, dx=None, dweight=None, dbias=None) == B.DSA3D_ERR_NULL_POINTER
+
+
+def test_conv_alignment_and_aliasing():
+    d = good_conv()
+    far = ptrs(16)[15]
+    assert conv_fwd(d, x=far + 4) == B.DSA3D_ERR_MISALIGNED      # fp32 pair needs 8 bytes
+    # bf16 needs only 4 bytes: with a NULL weight the call stops at the pointer check instead
+    assert conv_fwd(good_conv(dtype="bf16"), x=far + 4, weight=None) == B.DSA3D_ERR_NULL_POINTER
+    assert conv_fwd(good_conv(dtype="bf16"), y=far + 2) == B.DSA3D_ERR_MISALIGNED
+    assert conv_fwd(d, weight=far + 2) == B.DSA3D_ERR_MISALIGNED
+    assert conv_bwd(d, dx=far + 4) == B.DSA3D_ERR_MISALIGNED
+    assert conv_bwd(d, workspace=far + 128) == B.DSA3D_ERR_MISALIGNED
+    x = ptrs(1)[0]
+    assert conv_fwd(d, y=x) == B.DSA3D_ERR_ALIAS
+    assert conv_fwd(d, y=x + 64) == B.DSA3D_ERR_ALIAS
+    names = ptrs(7)
+    assert conv_bwd(d, dweight=names[3]) == B.DSA3D_ERR_ALIAS     # dweight == dx
+    assert conv_bwd(d, dx=names[2]) == B.DSA3D_ERR_ALIAS          # dx == dy
+    assert conv_bwd(d, workspace=names[5]) == B.DSA3D_ERR_ALIAS   # workspace == dbias
+
+
+def test_conv_workspace_size_and_errors():
+    for kw in (dict(), dict(B=2, T=7, H=300, W=9, C=258, kt=5, kh=1, kw=7),
+               dict(T=2, H=3, W=9, C=4000, kt=3)):
+        d = good_conv(**kw)
+        chunks = -(-d.channels // 128)
+        strips = -(-d.width // 8)
+        sg = min(strips, 5)
+        tiles_per_bc = -(-strips // sg) * sg * d.frames * -(-d.height // 4)
+        blocks = min(max(768 // (chunks * d.kt), 1), d.batch * tiles_per_bc)
+        taps = d.kt * d.kh * d.kw
+        slots = blocks * 4
+        r256 = lambda n: -(-n // 256) * 256
+        assert dsa.dsa3d_dwconv3d_backward_workspace_size(d) == \
+            r256(slots * d.channels * taps * 4) + r256(slots * d.channels * 4)
+    assert dsa.dsa3d_dwconv3d_backward_workspace_size(good_conv(kt=2)) == 0
+    d = good_conv()
+    need = dsa.dsa3d_dwconv3d_backward_workspace_size(d)
+    assert conv_bwd(d, workspace=None) == B.DSA3D_ERR_WORKSPACE
+    assert conv_bwd(d, workspace_bytes=need - 1) == B.DSA3D_ERR_WORKSPACE
+    # dx alone needs no workspace: the call passes validation up to the (absent) device,
+    # so only check that the workspace is not what fails
+    assert conv_bwd(d, workspace=None, dweight=None, dbias=None, dx=None) == \
+        B.DSA3D_ERR_NULL_POINTER
+
