@@ -62,6 +62,12 @@ def _load():
         lib.orc_backward_rows.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, vp, vp,
                                           ctypes.c_int64, vp, vp]
         lib.orc_backward_rows.restype = ctypes.c_int
+        lib.orc_pw_forward.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, ctypes.c_int64, vp,
+                                       vp]
+        lib.orc_pw_forward.restype = ctypes.c_int
+        lib.orc_pw_backward.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, ctypes.c_int64,
+                                        ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, vp, vp, vp]
+        lib.orc_pw_backward.restype = ctypes.c_int
         lib.orc_dwconv_forward.argtypes = [ctypes.POINTER(_Conv), vp, vp, vp, ctypes.c_int64,
                                            ctypes.c_int64, vp]
         lib.orc_dwconv_forward.restype = ctypes.c_int
@@ -182,6 +188,70 @@ def backward(shape, dtype, q, k, v, off, dout, scale=None):
             dk[b, :, :, :, m] = kk
             dv[b, :, :, :, m] = vv
     return dq, dk, dv, doff
+
+
+# ----------------------------------------------------------------------------- predicted weights
+
+def pw_forward(shape, dtype, logits, v, off, rows=None):
+    """Predicted-weights variant: output and LSE of the given flat rows (all if None), fp64.
+
+    logits float32 [B,T,H,W,heads,P]; v as in forward(); off float32 [..,heads,P,3]."""
+    pr = _problem(shape, dtype, 1.0)
+    v = _check_io(v, dtype)
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    off = np.ascontiguousarray(off, dtype=np.float32)
+    B, T, H, W, heads, D = shape[:6]
+    if rows is None:
+        rows = np.arange(B * T * H * W * heads, dtype=np.int64)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.empty((rows.size, D), dtype=np.float64)
+    lse = np.empty(rows.size, dtype=np.float64)
+    rc = _load().orc_pw_forward(ctypes.byref(pr), logits.ctypes.data, v.ctypes.data,
+                                off.ctypes.data, rows.ctypes.data, rows.size, out.ctypes.data,
+                                lse.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle pw forward: malformed problem")
+    return out, lse
+
+
+def pw_backward_slab(shape, dtype, logits, v, off, dout, b, m, t0, t1, dv=None):
+    """Predicted-weights variant: gradients from the queries of batch b, head m, frames
+    [t0, t1).  Returns (dlogits[(t1-t0),H,W,P], doff[(t1-t0),H,W,P,3], dv[T,H,W,D]); dv holds
+    only those queries' contributions (accumulated into the given array)."""
+    pr = _problem(shape, dtype, 1.0)
+    v, dout = _check_io(v, dtype), _check_io(dout, dtype)
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    off = np.ascontiguousarray(off, dtype=np.float32)
+    B, T, H, W, heads, D, kt, kh, kw = shape
+    P = kt * kh * kw
+    dlog = np.empty((t1 - t0, H, W, P), dtype=np.float64)
+    doff = np.empty((t1 - t0, H, W, P, 3), dtype=np.float64)
+    if dv is None:
+        dv = np.zeros((T, H, W, D), dtype=np.float64)
+    assert dv.flags["C_CONTIGUOUS"]
+    rc = _load().orc_pw_backward(ctypes.byref(pr), logits.ctypes.data, v.ctypes.data,
+                                 off.ctypes.data, dout.ctypes.data, b, m, t0, t1,
+                                 dlog.ctypes.data, doff.ctypes.data, dv.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle pw backward: malformed problem")
+    return dlog, doff, dv
+
+
+def pw_backward(shape, dtype, logits, v, off, dout):
+    """Full predicted-weights gradients: dlogits [B,T,H,W,heads,P], dv [B,T,H,W,heads,D],
+    doff [B,T,H,W,heads,P,3], fp64."""
+    B, T, H, W, heads, D, kt, kh, kw = shape
+    P = kt * kh * kw
+    dlog = np.empty((B, T, H, W, heads, P))
+    dv = np.empty((B, T, H, W, heads, D))
+    doff = np.empty((B, T, H, W, heads, P, 3))
+    for b in range(B):
+        for m in range(heads):
+            a, o, vv = pw_backward_slab(shape, dtype, logits, v, off, dout, b, m, 0, T)
+            dlog[b, :, :, :, m] = a
+            doff[b, :, :, :, m] = o
+            dv[b, :, :, :, m] = vv
+    return dlog, dv, doff
 
 
 # ----------------------------------------------------------------------------- depthwise conv

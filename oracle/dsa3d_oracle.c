@@ -365,3 +365,130 @@ int orc_backward_rows(const orc_problem* pr, const void* q, const void* k, const
   }
   return 0;
 }
+
+/*
+ * Predicted-weights variant.  Section 5.2 says the module learns offsets "and attention
+ * weights"; in this variant (as in Deformable DETR) the weights come from logits a_p that a
+ * linear layer predicts per (token, head, point), instead of from q.k:
+ *   alpha = softmax_p(a),  out = sum_p alpha_p v_p,  LSE = logsumexp_p(a)
+ * with v_p the same zero-padded trilinear sample of V.  There is no q and no K.
+ * Backward (same softmax calculus, no scale):
+ *   da_p = <dout, v_p>,  Delta = sum_p alpha_p da_p
+ *   d a_p          = alpha_p (da_p - Delta)
+ *   dV[corner c]  += alpha_p w_c dout
+ *   d dp_p[axis]   = alpha_p sum_c (d w_c / d pos[axis]) <dout, V[c]>
+ * logits, dlogits: [B][T][H][W][heads][P] (fp32 in, fp64 out here).
+ */
+static void pw_query(const orc_problem* pr, const float* logits, const void* v, const float* off,
+                     const void* dout, int64_t b, int64_t t, int64_t i, int64_t j, int64_t m,
+                     double* out, double* lse, double* dlog, double* doff, double* dv,
+                     orc_scratch* w) {
+  const int64_t P = pr->kt * pr->kh * pr->kw, D = pr->D;
+  const int64_t HW = pr->H * pr->W;
+  const int64_t row = row_of(pr, b, t, i, j, m);
+  double mx = -INFINITY;
+  for (int64_t p = 0; p < P; ++p) {
+    w->sp[p] = (double)logits[row * P + p];
+    mx = w->sp[p] > mx ? w->sp[p] : mx;
+  }
+  double l = 0.0;
+  for (int64_t p = 0; p < P; ++p) l += exp(w->sp[p] - mx);
+  for (int64_t p = 0; p < P; ++p) {
+    w->al[p] = exp(w->sp[p] - mx) / l;
+    sample_point(pr, b, t, i, j, m, p, off + (row * P + p) * 3, &w->pts[p]);
+    trilinear(pr, v, &w->pts[p], w->vp + p * D);
+  }
+  if (out) {
+    for (int64_t d = 0; d < D; ++d) {
+      double o = 0.0;
+      for (int64_t p = 0; p < P; ++p) o += w->al[p] * w->vp[p * D + d];
+      out[d] = o;
+    }
+  }
+  if (lse) *lse = mx + log(l);
+  if (!dlog && !doff && !dv) return;
+  for (int64_t d = 0; d < D; ++d) w->gv[d] = ld(dout, pr->bf16, row * D + d);
+  double delta = 0.0;
+  for (int64_t p = 0; p < P; ++p) {
+    double dd = 0.0;
+    for (int64_t d = 0; d < D; ++d) dd += w->gv[d] * w->vp[p * D + d];
+    w->da[p] = dd;
+    delta += w->al[p] * dd;
+  }
+  for (int64_t p = 0; p < P; ++p) {
+    const orc_point* s = &w->pts[p];
+    const double al = w->al[p];
+    if (dlog) dlog[p] = al * (w->da[p] - delta);
+    double g[3] = {0.0, 0.0, 0.0};
+    for (int c = 0; c < 8; ++c) {
+      if (!s->valid[c]) continue;
+      const int cx = c & 1, cy = (c >> 1) & 1, cz = (c >> 2) & 1;
+      const int64_t dst = ((s->crow[c] / pr->heads) % (pr->T * HW)) * D; /* (z,y,x) of batch b */
+      double dvv = 0.0;
+      for (int64_t d = 0; d < D; ++d) {
+        dvv += w->gv[d] * ld(v, pr->bf16, s->crow[c] * D + d);
+        if (dv) {
+          const double add = al * s->w[c] * w->gv[d];
+#pragma omp atomic
+          dv[dst + d] += add;
+        }
+      }
+      const double ax[2] = {1.0 - s->frac[0], s->frac[0]};
+      const double ay[2] = {1.0 - s->frac[1], s->frac[1]};
+      const double az[2] = {1.0 - s->frac[2], s->frac[2]};
+      g[0] += al * dvv * (cx ? 1.0 : -1.0) * ay[cy] * az[cz];
+      g[1] += al * dvv * (cy ? 1.0 : -1.0) * ax[cx] * az[cz];
+      g[2] += al * dvv * (cz ? 1.0 : -1.0) * ax[cx] * ay[cy];
+    }
+    if (doff)
+      for (int a = 0; a < 3; ++a) doff[p * 3 + a] = g[a];
+  }
+}
+
+/* Forward of the predicted-weights variant for a list of rows (as orc_forward). */
+int orc_pw_forward(const orc_problem* pr, const float* logits, const void* v, const float* off,
+                   const int64_t* rows, int64_t nrows, double* out, double* lse) {
+  const int64_t P = pr->kt * pr->kh * pr->kw, D = pr->D;
+  if (P <= 0 || D <= 0 || pr->kt % 2 == 0 || pr->kh % 2 == 0 || pr->kw % 2 == 0) return -1;
+#pragma omp parallel
+  {
+    orc_scratch w;
+    scratch_alloc(&w, P, D);
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int64_t row = rows[r];
+      const int64_t m = row % pr->heads, tok = row / pr->heads;
+      const int64_t j = tok % pr->W, i = (tok / pr->W) % pr->H, t = (tok / (pr->W * pr->H)) % pr->T;
+      const int64_t b = tok / (pr->W * pr->H * pr->T);
+      pw_query(pr, logits, v, off, NULL, b, t, i, j, m, out + r * D, lse ? lse + r : NULL, NULL,
+               NULL, NULL, &w);
+    }
+    scratch_free(&w);
+  }
+  return 0;
+}
+
+/* Backward of the predicted-weights variant for the queries of batch b, head m, frames
+ * [t0, t1): dlogits [(t1-t0)*H*W][P] and doff [..][P][3] overwritten; dv [T*H*W][D] of
+ * (b, m) ACCUMULATED from these queries. */
+int orc_pw_backward(const orc_problem* pr, const float* logits, const void* v, const float* off,
+                    const void* dout, int64_t b, int64_t m, int64_t t0, int64_t t1, double* dlog,
+                    double* doff, double* dv) {
+  const int64_t P = pr->kt * pr->kh * pr->kw, D = pr->D;
+  const int64_t HW = pr->H * pr->W;
+  if (P <= 0 || D <= 0 || t0 < 0 || t1 > pr->T || t0 > t1) return -1;
+  const int64_t nq = (t1 - t0) * HW;
+#pragma omp parallel
+  {
+    orc_scratch w;
+    scratch_alloc(&w, P, D);
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t n = 0; n < nq; ++n) {
+      const int64_t t = t0 + n / HW, i = (n % HW) / pr->W, j = n % pr->W;
+      pw_query(pr, logits, v, off, dout, b, t, i, j, m, NULL, NULL, dlog + n * P,
+               doff + n * P * 3, dv, &w);
+    }
+    scratch_free(&w);
+  }
+  return 0;
+}
