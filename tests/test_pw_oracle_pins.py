@@ -24,7 +24,8 @@ def case(seed, B, T, H, W, M, D, kt, kh, kw, off_std=1.0):
     rng = np.random.default_rng(seed)
     P = kt * kh * kw
     v = rng.standard_normal((B, T, H, W, M, D)).astype(np.float32)
-    logits = (2.0 * rng.standard_normal((B, T, H, W, M, P))).astype(np.float32)
+    # on a 2^-12 grid, so that adding a small constant to a row is exact in fp32
+    logits = (np.round(2.0 * rng.standard_normal((B, T, H, W, M, P)) * 4096) / 4096).astype(np.float32)
     off = (off_std * rng.standard_normal((B, T, H, W, M, P, 3))).astype(np.float32)
     dout = rng.standard_normal((B, T, H, W, M, D)).astype(np.float32)
     return v, logits, off, dout
@@ -116,7 +117,7 @@ def test_softmax_facts():
                 for p in range(len(g)):
                     x, y, z = np.array([j, i, t]) + g[p]
                     if 0 <= x < W and 0 <= y < H and 0 <= z < T:
-                        ref[t, i, j] += v[0, z, y, x] / len(g)
+                        ref[t, i, j] += v[0, z, y, x].astype(np.float64) / len(g)
     np.testing.assert_allclose(out3.reshape(ref.shape), ref, rtol=0, atol=1e-12)
 
 
@@ -132,5 +133,7 @@ def test_bf16_values_are_read_exactly():
     a = oracle.pw_backward(shape, "bf16", logits, vb, off, gb)
     b = oracle.pw_backward(shape, "f32", logits, testgen.bf16_to_f32(vb), off,
                            testgen.bf16_to_f32(gb))
-    for x, y in zip(a, b):
-        np.testing.assert_array_equal(x, y)
+    np.testing.assert_array_equal(a[0], b[0])   # dlogits: per query, fixed order
+    np.testing.assert_array_equal(a[2], b[2])   # d_offsets
+    # dV is scattered by OpenMP threads with atomic adds: only the summation order may differ
+    np.testing.assert_allclose(a[1], b[1], rtol=0, atol=1e-12)
