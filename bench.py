@@ -29,6 +29,8 @@ HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 VALU_PEAK_TFLOPS = 157.3        # MI355X fp32 vector peak (2 FLOP/lane/clk: dot2 / dual issue)
 DEFAULT_WORKLOAD = "fwdbwd_64x34x60"
 DEFAULT_CONV_WORKLOAD = "dwconv_1080p_256f"
+DEFAULT_PW_WORKLOAD = "pw_64x34x60"
+PW_METRIC = "3D-DSA predicted-weights fwd+bwd queries/s and achieved HBM GB/s (% of peak) at 1 GPU"
 CONV_METRIC = "DWConv3D fwd+bwd tokens/s and achieved HBM GB/s (% of peak) at 1 GPU"
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2607_22696_amd", "csrc")
@@ -302,14 +304,132 @@ def bench_dwconv(args, torch, dsa, testgen, to_device):
     print(json.dumps(res), flush=True)
 
 
+def pw_algorithmic(w):
+    """Per-launch algorithmic HBM bytes and FLOPs of the predicted-weights kernels, per query row
+    (s = bytes per V element, P points, head_dim D):
+      fwd_kernel           logits (4 P), offsets (12 P), V read and out written (2 D s), lse (4);
+                           8 P D multiply-adds (V at 8 corners)
+      bwd_sweep_kernel     logits, offsets, lse, V and dout read (2 D s + 16 P + 4);
+                           8 P D multiply-adds (dout.V at 8 corners)
+      bwd_finalize_kernel  offsets read, d_offsets and dlogits written (28 P)
+      bwd_gather_kernel    dout read, dV written (D s + 4 D); 8 P D multiply-adds
+    """
+    s = 2 if w.dtype == "bf16" else 4
+    rows, P, D = w.queries, w.P, w.head_dim
+    per = {
+        "fwd_kernel": (2 * D * s + 16 * P + 4, 16 * P * D),
+        "bwd_sweep_kernel": (2 * D * s + 16 * P + 4, 16 * P * D),
+        "bwd_finalize_kernel": (28 * P, 0),
+        "bwd_gather_kernel": (D * s + 4 * D, 16 * P * D),
+        "forward": (2 * D * s + 16 * P + 4, 16 * P * D),
+        "backward": (2 * D * s + 16 * P + 4 + 4 * D + 16 * P, 32 * P * D),
+    }
+    return {k: {"bytes": rows * b, "flops": rows * f} for k, (b, f) in per.items()}
+
+
+def bench_pw(args, torch, dsa, testgen, to_device):
+    """One step = forward and backward of the predicted-weights variant."""
+    w = testgen.PW_WORKLOADS[args.workload]
+    t_gen = time.perf_counter()
+    logits, v, off, dout = testgen.gen_pw_inputs(
+        w, progress=lambda m: print(m, file=sys.stderr, flush=True))
+    bf = w.dtype == "bf16"
+    ld_, vd, od, gd = (to_device(logits, False), to_device(v, bf), to_device(off, False),
+                       to_device(dout, bf))
+    t_gen = time.perf_counter() - t_gen
+    kern = (w.kt, w.kh, w.kw)
+    out, lse = dsa.pw_forward(ld_, vd, od, kernel=kern)
+    f32 = dict(dtype=torch.float32, device=vd.device)
+    grads = (torch.empty(logits.shape, **f32), torch.empty(v.shape, **f32),
+             torch.empty(off.shape, **f32))
+    need = dsa.dsa3d_pw_backward_workspace_size(dsa.make_desc(
+        w.B, w.T, w.H, w.W, w.heads, w.head_dim, w.kt, w.kh, w.kw, w.dtype))
+    workspace = torch.empty(need, dtype=torch.uint8, device=vd.device)
+
+    def new_events(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:
+            e.record()
+        return evs
+
+    K = args.steps
+    ev = [new_events(2) for _ in range(K)]
+    ph = [new_events(dsa.DSA3D_BACKWARD_PHASES + 1) for _ in range(K)]
+
+    def step(s=None):
+        if s is not None:
+            ev[s][0].record()
+        dsa.pw_forward(ld_, vd, od, kernel=kern, out=out, lse=lse)
+        if s is not None:
+            ev[s][1].record()
+        dsa.pw_backward(ld_, vd, od, lse, gd, kernel=kern, grads=grads, workspace=workspace,
+                        phase_events=None if s is None else ph[s])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for s in range(K):
+        step(s)
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / K
+    kernel_ms = {"fwd_kernel": sum(e[0].elapsed_time(e[1]) for e in ev) / K}
+    for i, n in enumerate(["bwd_sweep_kernel", "bin_scan", "bwd_finalize_kernel",
+                           "bwd_gather_kernel"]):
+        kernel_ms[n] = sum(p[i].elapsed_time(p[i + 1]) for p in ph) / K
+    alg = pw_algorithmic(w)
+    kname = max((n for n in kernel_ms if n in alg), key=lambda n: kernel_ms[n])
+    roof = roofline(alg[kname], kernel_ms[kname])
+    roof["traffic"] = None
+    roof["kernel"] = kname
+    roof["avg_launch_ms"] = round(kernel_ms[kname], 4)
+    step_bytes = alg["forward"]["bytes"] + alg["backward"]["bytes"]
+    res = {
+        "metric": PW_METRIC, "value": round(w.B * w.N / (ms_step * 1e-3), 1), "unit": "queries/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded Philox inputs shaped like the paper's video-latent grids)",
+        "config": {"workload": w.name, "grid_TxHxW": [w.T, w.H, w.W], "batch": w.B,
+                   "heads": w.heads, "head_dim": w.head_dim, "kernel": [w.kt, w.kh, w.kw],
+                   "points": w.P, "backward": True, "parallelism": "single GPU"},
+        "kernel_ms": {n: round(t, 4) for n, t in kernel_ms.items()},
+        "kernel_roofline": {n: roofline(alg[n], t) for n, t in kernel_ms.items() if n in alg},
+        "hbm_gbs_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": roof, "input_gen_s": round(t_gen, 1),
+    }
+    if args.cpu_budget > 0:
+        import numpy as np
+
+        import oracle
+        shape = (w.B, w.T, w.H, w.W, w.heads, w.head_dim, w.kt, w.kh, w.kw)
+        frames = 0
+        t0 = time.perf_counter()
+        while frames < w.T and time.perf_counter() - t0 < args.cpu_budget:
+            rows = (np.arange(w.H * w.W, dtype=np.int64) + frames * w.H * w.W) * w.heads
+            oracle.pw_forward(shape, w.dtype, logits, v, off, rows=rows)
+            oracle.pw_backward_slab(shape, w.dtype, logits, v, off, dout, 0, 0, frames, frames + 1)
+            frames += 1
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {
+            "value": frames * w.H * w.W / w.heads / dt, "unit": "queries/s",
+            "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"head 0 frames [0,{frames}) of {w.name}: forward + backward incl. dV "
+                      f"scatter, fp64, {dt:.1f} s; scaled to query tokens (all {w.heads} heads)"}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--op", choices=["dsa", "dwconv"], default="dsa",
+    ap.add_argument("--op", choices=["dsa", "dwconv", "pw"], default="dsa",
                     help="dsa: the 3D-DSA operator (default); dwconv: the depthwise 3D "
-                         "convolution term of Eq. (1) (workloads dwconv_*)")
+                         "convolution term of Eq. (1) (workloads dwconv_*); pw: the "
+                         "predicted-weights variant (workloads pw_*)")
     ap.add_argument("--workload", default=None,
                     help=f"default {DEFAULT_WORKLOAD} (dsa) or {DEFAULT_CONV_WORKLOAD} (dwconv)")
     ap.add_argument("--forward-only", action="store_true",
@@ -325,7 +445,8 @@ def main():
     args = ap.parse_args()
 
     if args.workload is None:
-        args.workload = DEFAULT_CONV_WORKLOAD if args.op == "dwconv" else DEFAULT_WORKLOAD
+        args.workload = {"dwconv": DEFAULT_CONV_WORKLOAD, "pw": DEFAULT_PW_WORKLOAD}.get(
+            args.op, DEFAULT_WORKLOAD)
     if args.pmc_summary:
         pmc_summary(args.workload, *args.pmc_summary, copy_mib=args.copy_probe or 1024)
         return
@@ -361,6 +482,9 @@ def main():
     dsa.load()
     if args.op == "dwconv":
         bench_dwconv(args, torch, dsa, testgen, to_device)
+        return
+    if args.op == "pw":
+        bench_pw(args, torch, dsa, testgen, to_device)
         return
     w = testgen.WORKLOADS[args.workload]
     do_bwd = w.backward and not args.forward_only

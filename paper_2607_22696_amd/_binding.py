@@ -33,7 +33,8 @@ DSA3D_DWCONV_MAX_TAPS = 128
 EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_timed",
             "dsa3d_backward_workspace_size", "dsa3d_status_string", "dsa3d_abi_version",
             "dsa3d_dwconv3d_forward", "dsa3d_dwconv3d_backward_workspace_size",
-            "dsa3d_dwconv3d_backward")
+            "dsa3d_dwconv3d_backward", "dsa3d_pw_forward", "dsa3d_pw_backward_workspace_size",
+            "dsa3d_pw_backward")
 
 
 class dsa3d_desc(ctypes.Structure):
@@ -75,6 +76,13 @@ def load():
         lib.dsa3d_backward_timed.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                              ctypes.c_size_t, vp, ctypes.POINTER(vp)]
         lib.dsa3d_backward_timed.restype = ctypes.c_int
+        lib.dsa3d_pw_forward.argtypes = [pd, vp, vp, vp, vp, vp, vp]
+        lib.dsa3d_pw_forward.restype = ctypes.c_int
+        lib.dsa3d_pw_backward_workspace_size.argtypes = [pd]
+        lib.dsa3d_pw_backward_workspace_size.restype = ctypes.c_size_t
+        lib.dsa3d_pw_backward.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp,
+                                          ctypes.POINTER(vp)]
+        lib.dsa3d_pw_backward.restype = ctypes.c_int
         cd = ctypes.POINTER(dsa3d_dwconv_desc)
         lib.dsa3d_dwconv3d_forward.argtypes = [cd, vp, vp, vp, vp, ctypes.c_int, vp]
         lib.dsa3d_dwconv3d_forward.restype = ctypes.c_int
@@ -152,18 +160,46 @@ def dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offset
                          check=True) -> int:
     """`events`: None or DSA3D_BACKWARD_PHASES + 1 torch.cuda.Event objects (or raw hipEvent_t
     addresses); each must already be created, i.e. recorded once."""
-    arr = None
-    if events is not None:
-        handles = [e if isinstance(e, int) else e.cuda_event for e in events]
-        if len(handles) != DSA3D_BACKWARD_PHASES + 1 or not all(handles):
-            raise ValueError("dsa3d_backward_timed needs DSA3D_BACKWARD_PHASES + 1 created events")
-        arr = (ctypes.c_void_p * len(handles))(*handles)
+    arr = _event_array(events)
     st = load().dsa3d_backward_timed(ctypes.byref(desc) if desc is not None else None, _ptr(q),
                                      _ptr(k), _ptr(v), _ptr(offsets), _ptr(lse), _ptr(dout),
                                      _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_offsets),
                                      _ptr(workspace), workspace_bytes, _stream(stream), arr)
     if check and st != DSA3D_OK:
         raise Dsa3dError(st, "dsa3d_backward_timed")
+    return st
+
+
+def dsa3d_pw_forward(desc, logits, v, offsets, out, lse=None, stream=None, check=True) -> int:
+    st = load().dsa3d_pw_forward(ctypes.byref(desc) if desc is not None else None, _ptr(logits),
+                                 _ptr(v), _ptr(offsets), _ptr(out), _ptr(lse), _stream(stream))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_pw_forward")
+    return st
+
+
+def dsa3d_pw_backward_workspace_size(desc) -> int:
+    return load().dsa3d_pw_backward_workspace_size(ctypes.byref(desc))
+
+
+def _event_array(events):
+    """None, or a ctypes array of DSA3D_BACKWARD_PHASES + 1 created event handles."""
+    if events is None:
+        return None
+    handles = [e if isinstance(e, int) else e.cuda_event for e in events]
+    if len(handles) != DSA3D_BACKWARD_PHASES + 1 or not all(handles):
+        raise ValueError("phase timing needs DSA3D_BACKWARD_PHASES + 1 created events")
+    return (ctypes.c_void_p * len(handles))(*handles)
+
+
+def dsa3d_pw_backward(desc, logits, v, offsets, lse, dout, dlogits, dv, d_offsets, workspace=None,
+                      workspace_bytes=0, stream=None, events=None, check=True) -> int:
+    st = load().dsa3d_pw_backward(ctypes.byref(desc) if desc is not None else None, _ptr(logits),
+                                  _ptr(v), _ptr(offsets), _ptr(lse), _ptr(dout), _ptr(dlogits),
+                                  _ptr(dv), _ptr(d_offsets), _ptr(workspace), workspace_bytes,
+                                  _stream(stream), _event_array(events))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_pw_backward")
     return st
 
 

@@ -1,6 +1,7 @@
 // C-ABI entry points of the 3D-DSA library: argument validation and kernel dispatch.
 // The operator and the conventions are described in include/dsa3d.h.
 #include "dsa3d.h"
+#include "dsa3d_pw.h"
 
 #include <hip/hip_runtime.h>
 
@@ -120,8 +121,8 @@ dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k,
     for (const Span& s : in)
       if (overlaps(sl, s)) return DSA3D_ERR_ALIAS;
   }
-  const hipError_t e = dsa3d::launch_forward(g, desc->dtype == DSA3D_BF16, q, k, v, offsets, out,
-                                             lse, static_cast<hipStream_t>(stream));
+  const hipError_t e = dsa3d::launch_forward(g, desc->dtype == DSA3D_BF16, q, k, v, nullptr,
+                                             offsets, out, lse, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
@@ -177,8 +178,9 @@ dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const v
   for (const Span& s : in)
     if (overlaps(sw, s)) return DSA3D_ERR_ALIAS;
   const hipError_t e = dsa3d::launch_backward(
-      g, desc->dtype == DSA3D_BF16, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace,
-      static_cast<hipStream_t>(stream), reinterpret_cast<hipEvent_t const*>(events));
+      g, desc->dtype == DSA3D_BF16, q, k, v, nullptr, offsets, lse, dout, dq, dk, dv, d_offsets,
+      nullptr, workspace, static_cast<hipStream_t>(stream),
+      reinterpret_cast<hipEvent_t const*>(events));
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
@@ -188,6 +190,98 @@ dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k
                             size_t workspace_bytes, void* stream) {
   return dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace,
                               workspace_bytes, stream, nullptr);
+}
+
+// ---------------------------------------------------------------------------- predicted weights
+
+// The variant takes its logits as given: a descriptor scale other than 0 or 1 is rejected.
+static dsa3d_status check_pw(const dsa3d_desc* desc, dsa3d::Geometry* g, uint64_t* rows,
+                             uint64_t* io_bytes, uint64_t* f32_bytes, uint64_t* off_bytes,
+                             uint64_t* logit_bytes) {
+  const dsa3d_status st = check_desc(desc, g, rows, io_bytes, f32_bytes, off_bytes);
+  if (st != DSA3D_OK) return st;
+  if (desc->scale != 0.0f && desc->scale != 1.0f) return DSA3D_ERR_INVALID_SHAPE;
+  g->scale = 1.0f;
+  g->scale_log2 = 1.4426950408889634f;
+  *logit_bytes = *rows * g->P * 4;
+  return DSA3D_OK;
+}
+
+dsa3d_status dsa3d_pw_forward(const dsa3d_desc* desc, const float* logits, const void* v,
+                              const float* offsets, void* out, float* lse, void* stream) {
+  dsa3d::Geometry g;
+  uint64_t rows, io_bytes, f32_bytes, off_bytes, logit_bytes;
+  dsa3d_status st = check_pw(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes, &logit_bytes);
+  if (st != DSA3D_OK) return st;
+  if (!logits || !v || !offsets || !out) return DSA3D_ERR_NULL_POINTER;
+  if (!aligned(v, 16) || !aligned(out, 16) || !aligned(logits, 4) || !aligned(offsets, 4) ||
+      (lse && !aligned(lse, 4)))
+    return DSA3D_ERR_MISALIGNED;
+  const Span in[] = {span_of(logits, logit_bytes), span_of(v, io_bytes),
+                     span_of(offsets, off_bytes)};
+  const Span so = span_of(out, io_bytes);
+  for (const Span& s : in)
+    if (overlaps(so, s)) return DSA3D_ERR_ALIAS;
+  if (lse) {
+    const Span sl = span_of(lse, rows * 4);
+    if (overlaps(sl, so)) return DSA3D_ERR_ALIAS;
+    for (const Span& s : in)
+      if (overlaps(sl, s)) return DSA3D_ERR_ALIAS;
+  }
+  // q and k are not read: v stands in for them so that every pointer the kernel forms is valid
+  const hipError_t e = dsa3d::launch_forward(g, desc->dtype == DSA3D_BF16, v, v, v, logits,
+                                             offsets, out, lse, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
+}
+
+size_t dsa3d_pw_backward_workspace_size(const dsa3d_desc* desc) {
+  dsa3d::Geometry g;
+  uint64_t rows, io_bytes, f32_bytes, off_bytes, logit_bytes;
+  if (check_pw(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes, &logit_bytes) != DSA3D_OK)
+    return 0;
+  if (check_backward_range(g, rows) != DSA3D_OK) return 0;
+  return dsa3d::backward_workspace_bytes(g);
+}
+
+dsa3d_status dsa3d_pw_backward(const dsa3d_desc* desc, const float* logits, const void* v,
+                               const float* offsets, const float* lse, const void* dout,
+                               float* dlogits, float* dv, float* d_offsets, void* workspace,
+                               size_t workspace_bytes, void* stream, void* const* events) {
+  dsa3d::Geometry g;
+  uint64_t rows, io_bytes, f32_bytes, off_bytes, logit_bytes;
+  dsa3d_status st = check_pw(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes, &logit_bytes);
+  if (st != DSA3D_OK) return st;
+  if (!logits || !v || !offsets || !lse || !dout || !dlogits || !dv || !d_offsets)
+    return DSA3D_ERR_NULL_POINTER;
+  st = check_backward_range(g, rows);
+  if (st != DSA3D_OK) return st;
+  const size_t ws_need = dsa3d::backward_workspace_bytes(g);
+  if (workspace == nullptr || workspace_bytes < ws_need) return DSA3D_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return DSA3D_ERR_MISALIGNED;
+  if (!aligned(v, 16) || !aligned(dout, 16) || !aligned(dv, 16) || !aligned(logits, 4) ||
+      !aligned(offsets, 4) || !aligned(lse, 4) || !aligned(dlogits, 4) || !aligned(d_offsets, 4))
+    return DSA3D_ERR_MISALIGNED;
+  const Span in[] = {span_of(logits, logit_bytes), span_of(v, io_bytes),
+                     span_of(offsets, off_bytes),  span_of(lse, rows * 4),
+                     span_of(dout, io_bytes)};
+  const Span outs[] = {span_of(dlogits, logit_bytes), span_of(dv, f32_bytes),
+                       span_of(d_offsets, off_bytes)};
+  const Span sw = span_of(workspace, ws_need);
+  for (int a = 0; a < 3; ++a) {
+    for (const Span& s : in)
+      if (overlaps(outs[a], s)) return DSA3D_ERR_ALIAS;
+    for (int b = a + 1; b < 3; ++b)
+      if (overlaps(outs[a], outs[b])) return DSA3D_ERR_ALIAS;
+    if (overlaps(outs[a], sw)) return DSA3D_ERR_ALIAS;
+  }
+  for (const Span& s : in)
+    if (overlaps(sw, s)) return DSA3D_ERR_ALIAS;
+  // q, k, dq and dk are not used: valid pointers stand in for them
+  const hipError_t e = dsa3d::launch_backward(
+      g, desc->dtype == DSA3D_BF16, dout, v, v, logits, offsets, lse, dout, dv, dv, dv, d_offsets,
+      dlogits, workspace, static_cast<hipStream_t>(stream),
+      reinterpret_cast<hipEvent_t const*>(events));
+  return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
 }  // extern "C"

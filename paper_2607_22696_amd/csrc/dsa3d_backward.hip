@@ -77,12 +77,16 @@ __device__ inline bool cell_inside(const Geometry& g, int x, int y, int z) {
 // the row's lanes pick the corner indices, fractions and cell up with ds_bpermute; the
 // weights are rebuilt from the fractions with the same products.  Lane `sub` also keeps
 // that point's record, and the row stores the chunk's records as one contiguous block.
-template <int D, bool BF16>
+//
+// PW (the predicted-weights variant): the logit of a point is given (`logits`), so q and the K
+// corners are not read, there is no dq, and A_p = 0 in the record.
+template <int D, bool BF16, bool PW>
 __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
-    const float* __restrict__ offsets, const float* __restrict__ lse,
-    const void* __restrict__ dout, float* __restrict__ dq, PointRec* __restrict__ recs,
-    float* __restrict__ delta_out, uint32_t* __restrict__ counts, int tiles) {
+    const float* __restrict__ logits, const float* __restrict__ offsets,
+    const float* __restrict__ lse, const void* __restrict__ dout, float* __restrict__ dq,
+    PointRec* __restrict__ recs, float* __restrict__ delta_out, uint32_t* __restrict__ counts,
+    int tiles) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -110,7 +114,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
     const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
-    const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
+    uint4 qr = make_uint4(0u, 0u, 0u, 0u);
+    if constexpr (!PW) qr = load16(qb, row * LY::kRowBytes + lane_off);
     const uint4 gr = load16(gb, row * LY::kRowBytes + lane_off);
     const float lse2 = lse[row] * kLog2e;
     const float* off = offsets + row * g.P * 3;
@@ -128,6 +133,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
       const int it = pm / khw, ih = (pm - it * khw) / g.kw, iw = pm - it * khw - ih * g.kw;
       Point mine;
       make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
+      float mylog2 = 0.0f;  // PW: this lane's point's logit, base 2
+      if constexpr (PW) mylog2 = logits[row * g.P + pm] * kLog2e;
       const bool own = p0 + sub < g.P;
       if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))  // result unused: no wait
         __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
@@ -163,7 +170,10 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
           for (int c = 0; c < 8; ++c) pt.w[c] = pt.ax[c & 1] * wyz[c >> 1];
         }
         uint4 kr[8], vr[8];
-        load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
+        if constexpr (PW)
+          load_rows<LY::kRowBytes>(g, win, win.v, vb, b, m, lane_off, pt, vr);
+        else
+          load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
         float sp = 0.0f, dap = 0.0f;
         float a3[3] = {0.0f, 0.0f, 0.0f}, b3[3] = {0.0f, 0.0f, 0.0f};
         float kp[VEC];
@@ -172,34 +182,43 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
           const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
-          const float qk = chunk_dot<BF16>(qr, kr[c]);
           const float dvv = chunk_dot<BF16>(gr, vr[c]);
-          sp = fmaf(pt.w[c], qk, sp);
           dap = fmaf(pt.w[c], dvv, dap);
           // d w_c / d pos along each axis (corners outside the grid have zero rows, so zero dots)
           const float wx = cx ? pt.ay[cy] * pt.az[cz] : -(pt.ay[cy] * pt.az[cz]);
           const float wy = cy ? pt.ax[cx] * pt.az[cz] : -(pt.ax[cx] * pt.az[cz]);
           const float wz = cz ? pt.ax[cx] * pt.ay[cy] : -(pt.ax[cx] * pt.ay[cy]);
-          a3[0] = fmaf(wx, qk, a3[0]);
-          a3[1] = fmaf(wy, qk, a3[1]);
-          a3[2] = fmaf(wz, qk, a3[2]);
           b3[0] = fmaf(wx, dvv, b3[0]);
           b3[1] = fmaf(wy, dvv, b3[1]);
           b3[2] = fmaf(wz, dvv, b3[2]);
-          chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
+          if constexpr (!PW) {
+            const float qk = chunk_dot<BF16>(qr, kr[c]);
+            sp = fmaf(pt.w[c], qk, sp);
+            a3[0] = fmaf(wx, qk, a3[0]);
+            a3[1] = fmaf(wy, qk, a3[1]);
+            a3[2] = fmaf(wz, qk, a3[2]);
+            chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
+          }
         }
-        const float alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
+        float alpha;
+        if constexpr (PW)
+          alpha = exp2f(__int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mylog2))) -
+                        lse2);
+        else
+          alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
         const float da = group_sum<L>(dap);
         delta = fmaf(alpha, da, delta);
-        const float ada = alpha * da;
+        if constexpr (!PW) {
+          const float ada = alpha * da;
 #pragma unroll
-        for (int x = 0; x < VEC; ++x) {
-          ak[x] = fmaf(ada, kp[x], ak[x]);
-          bk[x] = fmaf(alpha, kp[x], bk[x]);
+          for (int x = 0; x < VEC; ++x) {
+            ak[x] = fmaf(ada, kp[x], ak[x]);
+            bk[x] = fmaf(alpha, kp[x], bk[x]);
+          }
         }
 #pragma unroll
         for (int a = 0; a < 3; ++a) {
-          a3[a] = group_sum<L>(a3[a]);
+          if constexpr (!PW) a3[a] = group_sum<L>(a3[a]);
           b3[a] = group_sum<L>(b3[a]);
         }
         if (sub == kk) {
@@ -213,13 +232,15 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
         dst[1] = rec1;
       }
     }
-    float* dqr = dq + row * D + sub * VEC;
+    if constexpr (!PW) {
+      float* dqr = dq + row * D + sub * VEC;
 #pragma unroll
-    for (int x = 0; x < VEC; x += 4)
-      *reinterpret_cast<float4*>(dqr + x) =
+      for (int x = 0; x < VEC; x += 4)
+        *reinterpret_cast<float4*>(dqr + x) =
           make_float4(g.scale * fmaf(-delta, bk[x], ak[x]), g.scale * fmaf(-delta, bk[x + 1], ak[x + 1]),
                       g.scale * fmaf(-delta, bk[x + 2], ak[x + 2]),
-                      g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
+                        g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
+    }
     if (sub == 0) delta_out[row] = delta;
   }
 }
@@ -319,10 +340,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t
 
 // ---------------------------------------------------------------------------- 3. finalize
 
+// dlogits (the predicted-weights variant, else null) receives alpha_p (da_p - Delta).
 __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
     Geometry g, const float* __restrict__ offsets, const PointRec* __restrict__ recs,
     const float* __restrict__ delta, uint32_t* __restrict__ cursor, float* __restrict__ doff,
-    Entry* __restrict__ entries, int npoints) {
+    float* __restrict__ dlogits, Entry* __restrict__ entries, int npoints) {
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const unsigned P = g.P, heads = g.heads, N = g.N, W = g.W, HW = g.H * g.W;
   for (unsigned idx = blockIdx.x * blockDim.x + threadIdx.x; idx < (unsigned)npoints;
@@ -336,6 +358,7 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
     d[0] = r.alpha * fmaf(sa, r.ax, r.bx);
     d[1] = r.alpha * fmaf(sa, r.ay, r.by);
     d[2] = r.alpha * fmaf(sa, r.az, r.bz);
+    if (dlogits != nullptr) dlogits[idx] = r.alpha * dd;
     const unsigned tok = row / heads;
     const unsigned m = row - tok * heads;
     const unsigned b = tok / N;
@@ -384,7 +407,7 @@ struct BlockAcc {
 // upper of x0 and the lower of x0 + 1: [s0, m1), [m1, m2), [m2, end).  `zlow` says whether
 // the voxels are the lower z corner of this plane's cells.  Entries are read one batch
 // ahead, so a batch waits for its rows only.
-template <int D, bool BF16, int YR>
+template <int D, bool BF16, bool PW, int YR>
 __device__ inline __attribute__((always_inline)) void gather_run(
     const char* __restrict__ qh, const char* __restrict__ gh, uint32_t tok_bytes,
     const Entry* __restrict__ entries, uint32_t s0, uint32_t m1, uint32_t m2, uint32_t end,
@@ -401,7 +424,7 @@ __device__ inline __attribute__((always_inline)) void gather_run(
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const uint64_t o = (uint64_t)(uint32_t)en[k].n * tok_bytes;
-      qr[k] = *reinterpret_cast<const uint4*>(qh + o);
+      if constexpr (!PW) qr[k] = *reinterpret_cast<const uint4*>(qh + o);
       gr[k] = *reinterpret_cast<const uint4*>(gh + o);
     }
     Entry nx[U];
@@ -415,7 +438,7 @@ __device__ inline __attribute__((always_inline)) void gather_run(
       const float tx0 = wz * (uk < m1 ? en[k].fx : (uk < m2 ? lo : 0.0f));
       const float tx1 = wz * (uk < m1 ? 0.0f : (uk < m2 ? en[k].fx : lo));
       float qf[VEC], gf[VEC];
-      chunk_to_float<BF16>(qr[k], qf);
+      if constexpr (!PW) chunk_to_float<BF16>(qr[k], qf);
       chunk_to_float<BF16>(gr[k], gf);
 #pragma unroll
       for (int yi = 0; yi < 2; ++yi) {
@@ -426,8 +449,10 @@ __device__ inline __attribute__((always_inline)) void gather_run(
         const float k0 = sk * tx0, k1 = sk * tx1, v0 = sv * tx0, v1 = sv * tx1;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          acc.k[2 * yi][e] = fmaf(k0, qf[e], acc.k[2 * yi][e]);
-          acc.k[2 * yi + 1][e] = fmaf(k1, qf[e], acc.k[2 * yi + 1][e]);
+          if constexpr (!PW) {
+            acc.k[2 * yi][e] = fmaf(k0, qf[e], acc.k[2 * yi][e]);
+            acc.k[2 * yi + 1][e] = fmaf(k1, qf[e], acc.k[2 * yi + 1][e]);
+          }
           acc.v[2 * yi][e] = fmaf(v0, gf[e], acc.v[2 * yi][e]);
           acc.v[2 * yi + 1][e] = fmaf(v1, gf[e], acc.v[2 * yi + 1][e]);
         }
@@ -442,7 +467,8 @@ __device__ inline __attribute__((always_inline)) void gather_run(
 // block's voxels are corners of the points in the 3 x 3 cells (x0-1..x0+1, y0-1..y0+1) of
 // the planes z - 1 and z: six runs of three adjacent bins, and each entry's q and dout rows
 // are loaded once per run for all the voxels it feeds.
-template <int D, bool BF16>
+// PW (the predicted-weights variant): dV only (there is no K).
+template <int D, bool BF16, bool PW>
 __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ dout,
     const uint32_t* __restrict__ starts, const Entry* __restrict__ entries, float* __restrict__ dk,
@@ -492,9 +518,9 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_
         r[yr][3] = hasx1 ? starts[ci + 3] : r[yr][2];
       }
       const bool zlow = cz == 1;
-      gather_run<D, BF16, 0>(qh, gh, tok_bytes, entries, r[0][0], r[0][1], r[0][2], r[0][3], zlow, acc);
-      gather_run<D, BF16, 1>(qh, gh, tok_bytes, entries, r[1][0], r[1][1], r[1][2], r[1][3], zlow, acc);
-      gather_run<D, BF16, 2>(qh, gh, tok_bytes, entries, r[2][0], r[2][1], r[2][2], r[2][3], zlow, acc);
+      gather_run<D, BF16, PW, 0>(qh, gh, tok_bytes, entries, r[0][0], r[0][1], r[0][2], r[0][3], zlow, acc);
+      gather_run<D, BF16, PW, 1>(qh, gh, tok_bytes, entries, r[1][0], r[1][1], r[1][2], r[1][3], zlow, acc);
+      gather_run<D, BF16, PW, 2>(qh, gh, tok_bytes, entries, r[2][0], r[2][1], r[2][2], r[2][3], zlow, acc);
     }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -506,8 +532,9 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_
       float* dvr = dv + row * D + sub * VEC;
 #pragma unroll
       for (int e = 0; e < VEC; e += 4) {
-        *reinterpret_cast<float4*>(dkr + e) =
-            make_float4(acc.k[c][e], acc.k[c][e + 1], acc.k[c][e + 2], acc.k[c][e + 3]);
+        if constexpr (!PW)
+          *reinterpret_cast<float4*>(dkr + e) =
+              make_float4(acc.k[c][e], acc.k[c][e + 1], acc.k[c][e + 2], acc.k[c][e + 3]);
         *reinterpret_cast<float4*>(dvr + e) =
             make_float4(acc.v[c][e], acc.v[c][e + 1], acc.v[c][e + 2], acc.v[c][e + 3]);
       }
@@ -560,10 +587,12 @@ int grid_for(int64_t items, int per_block = kBlockThreads, int cap = 1 << 20) {
 }
 
 template <int D, bool BF16>
+// logits != null: the predicted-weights variant (q, k, dq and dk unused; dlogits written).
 hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const void* v,
-                        const float* off, const float* lse, const void* dout, float* dq, float* dk,
-                        float* dv, float* doff, void* workspace, hipStream_t s,
-                        hipEvent_t const* ev) {
+                        const float* logits, const float* off, const float* lse, const void* dout,
+                        float* dq, float* dk, float* dv, float* doff, float* dlogits,
+                        void* workspace, hipStream_t s, hipEvent_t const* ev) {
+  const bool pw = logits != nullptr;
   // phase marks for the caller's timing events (none when ev is null)
   auto mark = [&](int i) { return ev == nullptr ? hipSuccess : hipEventRecord(ev[i], s); };
   Workspace w = carve(g, workspace);
@@ -583,11 +612,13 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
   if ((e = mark(0)) != hipSuccess) return e;
   {
-    void* a[] = {(void*)&g,   (void*)&q,    (void*)&k,  (void*)&v,      (void*)&off,
-                 (void*)&lse, (void*)&dout, (void*)&dq, (void*)&w.recs, (void*)&w.delta,
-                 (void*)&w.counts, (void*)&tiles};
-    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16>), dim3(blocks),
-                        dim3(kBlockThreads), a, 0, s);
+    void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,       (void*)&v,
+                 (void*)&logits, (void*)&off,  (void*)&lse,     (void*)&dout,
+                 (void*)&dq,   (void*)&w.recs, (void*)&w.delta, (void*)&w.counts,
+                 (void*)&tiles};
+    const void* kern = pw ? reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, true>)
+                          : reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, false>);
+    e = hipLaunchKernel(kern, dim3(blocks), dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   }
   if ((e = mark(1)) != hipSuccess) return e;
@@ -610,8 +641,9 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   if ((e = mark(2)) != hipSuccess) return e;
   {
     const int npoints = (int)points;
-    void* a[] = {(void*)&g,        (void*)&off,   (void*)&w.recs, (void*)&w.delta,
-                 (void*)&w.cursor, (void*)&doff,  (void*)&w.entries, (void*)&npoints};
+    void* a[] = {(void*)&g,      (void*)&off,     (void*)&w.recs,    (void*)&w.delta,
+                 (void*)&w.cursor, (void*)&doff, (void*)&dlogits, (void*)&w.entries,
+                 (void*)&npoints};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_finalize_kernel), dim3(grid_for(points)),
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
@@ -624,8 +656,9 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     const int gblocks = gtiles < kMaxBlocks ? gtiles : kMaxBlocks;
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
                  (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&gtiles};
-    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16>), dim3(gblocks),
-                        dim3(kBlockThreads), a, 0, s);
+    const void* kern = pw ? reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16, true>)
+                          : reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16, false>);
+    e = hipLaunchKernel(kern, dim3(gblocks), dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   }
   return mark(4);
@@ -636,12 +669,13 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
 size_t backward_workspace_bytes(const Geometry& g) { return carve(g, nullptr).bytes; }
 
 hipError_t launch_backward(const Geometry& g, bool bf16, const void* q, const void* k,
-                           const void* v, const float* offsets, const float* lse, const void* dout,
-                           float* dq, float* dk, float* dv, float* d_offsets, void* workspace,
-                           hipStream_t stream, hipEvent_t const* events) {
-#define DSA3D_BWD(DIM, BF) \
-  bwd_dispatch<DIM, BF>(g, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace, stream, \
-                         events)
+                           const void* v, const float* logits, const float* offsets,
+                           const float* lse, const void* dout, float* dq, float* dk, float* dv,
+                           float* d_offsets, float* dlogits, void* workspace, hipStream_t stream,
+                           hipEvent_t const* events) {
+#define DSA3D_BWD(DIM, BF)                                                                      \
+  bwd_dispatch<DIM, BF>(g, q, k, v, logits, offsets, lse, dout, dq, dk, dv, d_offsets, dlogits, \
+                        workspace, stream, events)
   switch (g.D) {
     case 32:
       return bf16 ? DSA3D_BWD(32, true) : DSA3D_BWD(32, false);

@@ -24,10 +24,14 @@ using namespace dev;
 // lane `sub` of a row computes point chunk + sub once, and the row's lanes pick each
 // point's corner indices, weights and cell up with ds_bpermute (the LDS crossbar: no VALU
 // work and no LDS storage) instead of every lane repeating the same arithmetic.
-template <int D, bool BF16>
+//
+// PW (the predicted-weights variant): the logit of a point is given (`logits`, one fp32 per
+// (row, point)) instead of scale <q, k_p>, so neither q nor the K corners are read.
+template <int D, bool BF16, bool PW>
 __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
-    const float* __restrict__ offsets, void* __restrict__ out, float* __restrict__ lse, int tiles) {
+    const float* __restrict__ logits, const float* __restrict__ offsets, void* __restrict__ out,
+    float* __restrict__ lse, int tiles) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -53,7 +57,8 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
     const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
-    const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
+    uint4 qr = make_uint4(0u, 0u, 0u, 0u);
+    if constexpr (!PW) qr = load16(qb, row * LY::kRowBytes + lane_off);
     const float* off = offsets + row * g.P * 3;
     float o[VEC];
 #pragma unroll
@@ -67,6 +72,8 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
       Point mine;
       make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, off[3 * pm], off[3 * pm + 1],
                  off[3 * pm + 2], mine);
+      float mylog2 = 0.0f;  // PW: this lane's point's logit, base 2
+      if constexpr (PW) mylog2 = logits[row * g.P + pm] * kLog2e;
       const int nk = min(L, g.P - p0);
       for (int kk = 0; kk < nk; ++kk) {
         const int src = (grp * L + kk) << 2;
@@ -80,12 +87,19 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
         pt.cy = __builtin_amdgcn_ds_bpermute(src, mine.cy);
         pt.cz = __builtin_amdgcn_ds_bpermute(src, mine.cz);
         pt.slow = __builtin_amdgcn_ds_bpermute(src, (int)mine.slow) != 0;
-        uint4 kr[8], vr[8];
-        load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
-        float sp = 0.0f;
+        uint4 vr[8];
+        float s2;
+        if constexpr (PW) {
+          load_rows<LY::kRowBytes>(g, win, win.v, vb, b, m, lane_off, pt, vr);
+          s2 = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mylog2)));
+        } else {
+          uint4 kr[8];
+          load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
+          float sp = 0.0f;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) sp = fmaf(pt.w[c], chunk_dot<BF16>(qr, kr[c]), sp);
-        const float s2 = group_sum<L>(sp) * g.scale_log2;
+          for (int c = 0; c < 8; ++c) sp = fmaf(pt.w[c], chunk_dot<BF16>(qr, kr[c]), sp);
+          s2 = group_sum<L>(sp) * g.scale_log2;
+        }
         // One exponential per point: a new maximum rescales the running sums by
         // 2^(old max - new max) and enters with weight exactly 1; otherwise the point enters
         // with 2^(s - max).  (The first point always takes the first branch: 2^-inf = 0.)
@@ -123,33 +137,30 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
 
 template <int D, bool BF16>
 hipError_t fwd_dispatch(const Geometry& g, const void* q, const void* k, const void* v,
-                        const float* off, void* out, float* lse, hipStream_t s) {
+                        const float* logits, const float* off, void* out, float* lse,
+                        hipStream_t s) {
   const int tiles = tiles_for<D, BF16>(g);
   const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
-  void* args[] = {(void*)&g, (void*)&q, (void*)&k, (void*)&v, (void*)&off, (void*)&out, (void*)&lse,
-                  (void*)&tiles};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&fwd_kernel<D, BF16>), dim3(blocks),
-                         dim3(kBlockThreads), args, 0, s);
+  void* args[] = {(void*)&g,   (void*)&q,   (void*)&k,   (void*)&v,    (void*)&logits,
+                  (void*)&off, (void*)&out, (void*)&lse, (void*)&tiles};
+  const void* kern = logits != nullptr ? reinterpret_cast<const void*>(&fwd_kernel<D, BF16, true>)
+                                       : reinterpret_cast<const void*>(&fwd_kernel<D, BF16, false>);
+  return hipLaunchKernel(kern, dim3(blocks), dim3(kBlockThreads), args, 0, s);
 }
 
 }  // namespace
 
 hipError_t launch_forward(const Geometry& g, bool bf16, const void* q, const void* k,
-                          const void* v, const float* offsets, void* out, float* lse,
-                          hipStream_t stream) {
+                          const void* v, const float* logits, const float* offsets, void* out,
+                          float* lse, hipStream_t stream) {
+#define DSA3D_FWD(DIM, BF) fwd_dispatch<DIM, BF>(g, q, k, v, logits, offsets, out, lse, stream)
   switch (g.D) {
-    case 32:
-      return bf16 ? fwd_dispatch<32, true>(g, q, k, v, offsets, out, lse, stream)
-                  : fwd_dispatch<32, false>(g, q, k, v, offsets, out, lse, stream);
-    case 64:
-      return bf16 ? fwd_dispatch<64, true>(g, q, k, v, offsets, out, lse, stream)
-                  : fwd_dispatch<64, false>(g, q, k, v, offsets, out, lse, stream);
-    case 128:
-      return bf16 ? fwd_dispatch<128, true>(g, q, k, v, offsets, out, lse, stream)
-                  : fwd_dispatch<128, false>(g, q, k, v, offsets, out, lse, stream);
-    default:
-      return hipErrorInvalidValue;
+    case 32: return bf16 ? DSA3D_FWD(32, true) : DSA3D_FWD(32, false);
+    case 64: return bf16 ? DSA3D_FWD(64, true) : DSA3D_FWD(64, false);
+    case 128: return bf16 ? DSA3D_FWD(128, true) : DSA3D_FWD(128, false);
+    default: return hipErrorInvalidValue;
   }
+#undef DSA3D_FWD
 }
 
 }  // namespace dsa3d

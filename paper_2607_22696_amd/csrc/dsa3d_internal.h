@@ -22,17 +22,21 @@ struct Geometry {
 int window_frames(const Geometry& g, int row_bytes);
 
 // All launches return the hipError_t of the launch itself.
+// logits != null: the predicted-weights variant (q and k are not read; pass valid pointers).
 hipError_t launch_forward(const Geometry& g, bool bf16, const void* q, const void* k,
-                          const void* v, const float* offsets, void* out, float* lse,
-                          hipStream_t stream);
+                          const void* v, const float* logits, const float* offsets, void* out,
+                          float* lse, hipStream_t stream);
 
 // Device workspace (bytes) the backward needs for this geometry.
 size_t backward_workspace_bytes(const Geometry& g);
 
+// logits != null: the predicted-weights variant (q, k, dq, dk are not used; pass valid
+// pointers for q and k; dlogits receives alpha_p (da_p - Delta)).
 hipError_t launch_backward(const Geometry& g, bool bf16, const void* q, const void* k,
-                           const void* v, const float* offsets, const float* lse, const void* dout,
-                           float* dq, float* dk, float* dv, float* d_offsets, void* workspace,
-                           hipStream_t stream, hipEvent_t const* events);
+                           const void* v, const float* logits, const float* offsets,
+                           const float* lse, const void* dout, float* dq, float* dk, float* dv,
+                           float* d_offsets, float* dlogits, void* workspace, hipStream_t stream,
+                           hipEvent_t const* events);
 
 // ---------------------------------------------------------------------------- depthwise conv
 

@@ -9,7 +9,9 @@ import torch
 
 from ._binding import (dsa3d_backward, dsa3d_backward_timed, dsa3d_backward_workspace_size,
                        dsa3d_dwconv3d_backward, dsa3d_dwconv3d_backward_workspace_size,
-                       dsa3d_dwconv3d_forward, dsa3d_forward, make_conv_desc, make_desc)
+                       dsa3d_dwconv3d_forward, dsa3d_forward, dsa3d_pw_backward,
+                       dsa3d_pw_backward_workspace_size, dsa3d_pw_forward, make_conv_desc,
+                       make_desc)
 
 
 def _desc(q, kernel, scale):
@@ -112,4 +114,33 @@ def dwconv3d_backward(x, weight, dy, need_dx=True, need_dweight=True, need_dbias
             workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     dsa3d_dwconv3d_backward(desc, x, weight, dy, dx, dw, db, workspace, need, accumulate_dx)
     return dx, dw, db
+
+
+def pw_forward(logits, v, offsets, kernel=(3, 3, 3), need_lse=True, out=None, lse=None):
+    """Predicted-weights variant: softmax over the given logits [B,T,H,W,heads,P] (fp32)
+    instead of q.k.  Returns (out, lse)."""
+    desc = _desc(v, kernel, 0.0)
+    if out is None:
+        out = torch.empty_like(v)
+    if need_lse and lse is None:
+        lse = torch.empty(v.shape[:-1], dtype=torch.float32, device=v.device)
+    dsa3d_pw_forward(desc, logits, v, offsets, out, lse if need_lse else None)
+    return out, lse
+
+
+def pw_backward(logits, v, offsets, lse, dout, kernel=(3, 3, 3), grads=None, workspace=None,
+                phase_events=None):
+    """Returns (dlogits, dv, d_offsets), float32.  `phase_events` as for backward()."""
+    desc = _desc(v, kernel, 0.0)
+    if grads is None:
+        f32 = dict(dtype=torch.float32, device=v.device)
+        grads = (torch.empty(logits.shape, **f32), torch.empty(v.shape, **f32),
+                 torch.empty(offsets.shape, **f32))
+    dlog, dv, doff = grads
+    need = dsa3d_pw_backward_workspace_size(desc)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=v.device)
+    dsa3d_pw_backward(desc, logits, v, offsets, lse, dout, dlog, dv, doff, workspace, need,
+                      events=phase_events)
+    return dlog, dv, doff
 

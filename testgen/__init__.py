@@ -19,7 +19,7 @@ _SRC = os.path.join(_HERE, "testgen.c")
 _LIB = os.path.join(_HERE, "libtestgen.so")
 
 # Tensor ids (part of the counter); fixed so every slab is reproducible.
-TID_Q, TID_K, TID_V, TID_OFF, TID_DOUT = 0, 1, 2, 3, 4
+TID_Q, TID_K, TID_V, TID_OFF, TID_DOUT, TID_LOGITS = 0, 1, 2, 3, 4, 5
 
 NORMAL, UNIFORM = 0, 1
 
@@ -138,6 +138,9 @@ class Workload:
     def off_shape(self):
         return (self.B, self.T, self.H, self.W, self.heads, self.P, 3)
 
+    def logits_shape(self):
+        return (self.B, self.T, self.H, self.W, self.heads, self.P)
+
     def np_io_dtype(self):
         return np.float32 if self.dtype == "f32" else np.uint16
 
@@ -193,6 +196,35 @@ def gen_inputs(w: Workload, progress=None):
     off = one("offsets", TID_OFF, w.off_shape(), w.offsets, False)
     dout = one("dout", TID_DOUT, w.qkv_shape(), w.dout, True) if w.backward else None
     return q, k, v, off, dout
+
+
+# ----------------------------------------------------------------------------- predicted weights
+
+# Logits of the predicted-weights variant (the output of a linear layer): N(0, 1.5^2), so that
+# the softmax over the points is neither flat nor one-hot.
+PW_LOGITS = Dist(NORMAL, 0.0, 1.5)
+
+
+def gen_pw_inputs(w: Workload, progress=None):
+    """Host copies for the predicted-weights variant: logits (fp32), v (io dtype), offsets
+    (fp32) and dout (io dtype); v, offsets and dout are the tensors gen_inputs draws."""
+    def one(name, tid, shape, dist, io):
+        if progress is not None:
+            progress(f"generating {name} {shape} of {w.name}")
+        return gen_tensor(w, tid, shape, dist, io)
+
+    logits = one("logits", TID_LOGITS, w.logits_shape(), PW_LOGITS, False)
+    v = one("v", TID_V, w.qkv_shape(), w.qkv, True)
+    off = one("offsets", TID_OFF, w.off_shape(), w.offsets, False)
+    dout = one("dout", TID_DOUT, w.qkv_shape(), w.dout, True)
+    return logits, v, off, dout
+
+
+PW_WORKLOADS = {
+    # forward + backward of the predicted-weights variant on the forward + backward grid
+    "pw_64x34x60": Workload("pw_64x34x60", 1, 64, 34, 60, 16, 64, 3, 3, 3, "bf16", N01,
+                            Dist(UNIFORM, -2.0, 2.0), seed=7, backward=True),
+}
 
 
 # ----------------------------------------------------------------------------- depthwise conv

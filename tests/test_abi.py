@@ -302,3 +302,49 @@ def test_conv_workspace_size_and_errors():
     assert conv_bwd(d, workspace=None, dweight=None, dbias=None, dx=None) == \
         B.DSA3D_ERR_NULL_POINTER
 
+
+
+# ----------------------------------------------------------------------------- predicted weights
+
+def pw_fwd(desc, **over):
+    lg, v, off, out, lse = ptrs(5)
+    args = dict(logits=lg, v=v, offsets=off, out=out, lse=lse)
+    args.update(over)
+    return dsa.dsa3d_pw_forward(desc, args["logits"], args["v"], args["offsets"], args["out"],
+                                args["lse"], stream=0, check=False)
+
+
+def pw_bwd(desc, **over):
+    names = ["logits", "v", "offsets", "lse", "dout", "dlogits", "dv", "d_offsets", "workspace"]
+    args = dict(zip(names, ptrs(len(names))))
+    args["workspace_bytes"] = 1 << 33
+    args.update(over)
+    return dsa.dsa3d_pw_backward(desc, *[args[n] for n in names[:-1]], workspace=args["workspace"],
+                                 workspace_bytes=args["workspace_bytes"], stream=0, check=False)
+
+
+def test_pw_validation():
+    d = good_desc()
+    assert pw_fwd(good_desc(kt=2)) == B.DSA3D_ERR_INVALID_SHAPE
+    assert pw_fwd(good_desc(scale=0.5)) == B.DSA3D_ERR_INVALID_SHAPE   # logits are used as given
+    assert pw_fwd(good_desc(scale=1.0), logits=None) == B.DSA3D_ERR_NULL_POINTER
+    for name in ["logits", "v", "offsets", "out"]:
+        assert pw_fwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+    far = ptrs(16)[15]
+    assert pw_fwd(d, v=far + 8) == B.DSA3D_ERR_MISALIGNED
+    assert pw_fwd(d, logits=far + 2) == B.DSA3D_ERR_MISALIGNED
+    assert pw_fwd(d, out=ptrs(1)[0] + 256) == B.DSA3D_ERR_ALIAS        # out inside logits
+    for name in ["logits", "v", "offsets", "lse", "dout", "dlogits", "dv", "d_offsets"]:
+        assert pw_bwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+    names = ptrs(9)
+    assert pw_bwd(d, dv=names[5]) == B.DSA3D_ERR_ALIAS                 # dv == dlogits
+    assert pw_bwd(d, workspace=None) == B.DSA3D_ERR_WORKSPACE
+    assert pw_bwd(d, workspace=far + 128) == B.DSA3D_ERR_MISALIGNED
+    assert pw_bwd(d, dlogits=far + 2) == B.DSA3D_ERR_MISALIGNED
+
+
+def test_pw_workspace_is_the_backward_binning():
+    for kw in (dict(), dict(B=2, T=5, H=7, W=9, heads=3, kt=3, kh=5, kw=5)):
+        d = good_desc(**kw)
+        assert dsa.dsa3d_pw_backward_workspace_size(d) == dsa.dsa3d_backward_workspace_size(d) > 0
+    assert dsa.dsa3d_pw_backward_workspace_size(good_desc(scale=2.0)) == 0

@@ -1,0 +1,133 @@
+"""GPU-vs-oracle parity of the predicted-weights variant (Section 5.2: offsets and attention
+weights both predicted; softmax over given per-point logits, no q and no K), through the C ABI.
+
+Tolerances as for the main operator: fp32 data max-abs <= 1e-5 on every output and gradient;
+bf16 V / dout (fp32 accumulate) the relative metric <= 2e-2 against the fp64 oracle.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import testgen
+from tests.util import max_abs, reach_frames, rel_err, say, to_device, to_host
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-5
+BF16_TOL = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_22696_amd as dsa
+    dsa.load()
+    yield
+
+
+def check(name, got, ref, bf16):
+    if bf16:
+        e = rel_err(got, ref)
+        say(f"  {name}: rel {e:.3e} (max-abs {max_abs(got, ref):.3e})")
+        assert e <= BF16_TOL, name
+    else:
+        e = max_abs(got, ref)
+        say(f"  {name}: max-abs {e:.3e}")
+        assert e <= F32_TOL, name
+
+
+def shape9(w):
+    return (w.B, w.T, w.H, w.W, w.heads, w.head_dim, w.kt, w.kh, w.kw)
+
+
+def run(w, host=None):
+    import paper_2607_22696_amd as dsa
+    bf = w.dtype == "bf16"
+    logits, v, off, dout = host if host is not None else testgen.gen_pw_inputs(w)
+    ld_, vd, od, gd = (to_device(logits, False), to_device(v, bf), to_device(off, False),
+                       to_device(dout, bf))
+    kern = (w.kt, w.kh, w.kw)
+    out, lse = dsa.pw_forward(ld_, vd, od, kernel=kern)
+    dl, dv, doff = dsa.pw_backward(ld_, vd, od, lse, gd, kernel=kern)
+    torch.cuda.synchronize()
+    return out, lse, dl, dv, doff
+
+
+def small(name, **kw):
+    base = testgen.PW_WORKLOADS["pw_64x34x60"]
+    return base.with_grid(name=name, **kw)
+
+
+SMALL = [
+    small("pw_f32_tiny", T=4, H=8, W=8, heads=2, head_dim=32, dtype="f32", seed=40,
+          offsets=testgen.Dist(testgen.NORMAL, 0.0, 0.5)),
+    small("pw_bf16_ragged", T=5, H=9, W=11, heads=3, head_dim=64, dtype="bf16", seed=41),
+    small("pw_bf16_d128_3x5x5", T=4, H=7, W=9, heads=2, head_dim=128, dtype="bf16", kh=5, kw=5,
+          seed=42, offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
+    small("pw_f32_d64_1x3x3", T=3, H=10, W=6, heads=2, head_dim=64, dtype="f32", kt=1, seed=43),
+]
+
+
+@pytest.mark.parametrize("w", SMALL, ids=lambda w: w.name)
+def test_small_grid_parity(w):
+    bf = w.dtype == "bf16"
+    host = testgen.gen_pw_inputs(w)
+    logits, v, off, dout = host
+    out, lse, dl, dv, doff = run(w, host)
+    ro, rl = oracle.pw_forward(shape9(w), w.dtype, logits, v, off)
+    rdl, rdv, rdo = oracle.pw_backward(shape9(w), w.dtype, logits, v, off, dout)
+    check("out", to_host(out).reshape(ro.shape), ro, bf)
+    check("lse", to_host(lse).reshape(-1), rl, bf)
+    check("dlogits", to_host(dl), rdl, bf)
+    check("dv", to_host(dv), rdv, bf)
+    check("d_offsets", to_host(doff), rdo, bf)
+
+
+def test_single_point_integer_offsets_copy_rows_bitwise():
+    """One point with an integer offset: alpha = 1 and one corner of weight 1, so the output is
+    the V row at the offset position bit for bit (zero outside the grid)."""
+    w = small("pw_copy", T=3, H=5, W=6, heads=2, head_dim=64, dtype="bf16", kt=1, kh=1, kw=1,
+              seed=44)
+    logits, v, _, dout = testgen.gen_pw_inputs(w)
+    rng = np.random.default_rng(44)
+    off = rng.integers(-1, 2, w.off_shape()).astype(np.float32)
+    out, _, _, _, _ = run(w, (logits, v, off, dout))
+    got = to_host(out)
+    vf = testgen.bf16_to_f32(v)
+    ref = np.zeros_like(vf)
+    for t in range(w.T):
+        for i in range(w.H):
+            for j in range(w.W):
+                for m in range(w.heads):
+                    x, y, z = j + int(off[0, t, i, j, m, 0, 0]), i + int(off[0, t, i, j, m, 0, 1]), \
+                        t + int(off[0, t, i, j, m, 0, 2])
+                    if 0 <= x < w.W and 0 <= y < w.H and 0 <= z < w.T:
+                        ref[0, t, i, j, m] = vf[0, z, y, x, m]
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.slow
+def test_pw_64x34x60_full_size():
+    """130,560 tokens x 16 heads x 64, bf16, 27 points: the launch configuration the bench
+    times; 4096 sampled rows (out, lse, dlogits, d_offsets) and dV frame slabs."""
+    w = testgen.PW_WORKLOADS["pw_64x34x60"]
+    logits, v, off, dout = testgen.gen_pw_inputs(w, progress=say)
+    out, lse, dl, dv, doff = run(w, (logits, v, off, dout))
+    rng = np.random.default_rng(w.seed)
+    rows = np.unique(rng.choice(w.queries, size=4096, replace=False))
+    ro, rl = oracle.pw_forward(shape9(w), w.dtype, logits, v, off, rows=rows)
+    sel = torch.from_numpy(rows).cuda()
+    check("out[sampled rows]", to_host(out.view(-1, w.head_dim)[sel]), ro, True)
+    check("lse[sampled rows]", to_host(lse.view(-1)[sel]), rl, True)
+    R = reach_frames(w, float(np.max(np.abs(off[..., 2]))))
+    for m, f in [(0, 0), (7, 31), (15, 63)]:
+        t0, t1 = max(0, f - R), min(w.T, f + 1 + R)
+        say(f"  oracle backward head {m}, frames [{t0},{t1}) for dV at frame {f} ...")
+        rdl, rdo, rdv = oracle.pw_backward_slab(shape9(w), w.dtype, logits, v, off, dout, 0, m,
+                                                t0, t1)
+        check(f"dv[frame {f}, head {m}]", to_host(dv[0, f, :, :, m]), rdv[f], True)
+        check(f"dlogits[frames {t0}-{t1}, head {m}]", to_host(dl[0, t0:t1, :, :, m]), rdl, True)
+        check(f"d_offsets[frames {t0}-{t1}, head {m}]", to_host(doff[0, t0:t1, :, :, m]), rdo, True)
