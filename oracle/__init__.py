@@ -2,9 +2,10 @@
 
 TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
 bench's CPU-baseline leg may import this package.  It wraps ``dsa3d_oracle.c``
-(the attention term) and ``dwconv3d_oracle.c`` (the depthwise 3D convolution term
-and the offset network's depthwise convolution), plain C with fp64 accumulation and
-OpenMP, with ctypes, and shares nothing with the GPU library.  The arithmetic and
+(the attention term and its predicted-weights variant), ``dwconv3d_oracle.c`` (the
+depthwise 3D convolution term and the offset network's depthwise convolution) and
+``winattn_oracle.c`` (the Swin-DiT baseline's shifted-window attention), plain C with fp64
+accumulation and OpenMP, with ctypes, and shares nothing with the GPU library.  The arithmetic and
 the readings it follows are described at the top of each C file.
 """
 from __future__ import annotations
@@ -17,7 +18,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = [os.path.join(_HERE, "dsa3d_oracle.c"), os.path.join(_HERE, "dwconv3d_oracle.c")]
+_SRCS = [os.path.join(_HERE, "dsa3d_oracle.c"), os.path.join(_HERE, "dwconv3d_oracle.c"),
+         os.path.join(_HERE, "winattn_oracle.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 
@@ -44,6 +46,12 @@ class _Conv(ctypes.Structure):
                 ("pad_", ctypes.c_int32)]
 
 
+class _Win(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("B", "T", "H", "W", "heads", "D", "wt", "wh", "ww",
+                                              "st", "sh", "sw")] + \
+               [("scale", ctypes.c_double), ("bf16", ctypes.c_int32), ("pad_", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -68,6 +76,11 @@ def _load():
         lib.orc_pw_backward.argtypes = [ctypes.POINTER(_Problem), vp, vp, vp, vp, ctypes.c_int64,
                                         ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, vp, vp, vp]
         lib.orc_pw_backward.restype = ctypes.c_int
+        W = ctypes.POINTER(_Win)
+        lib.orc_win_forward.argtypes = [W, vp, vp, vp, ctypes.c_int64, ctypes.c_int64, vp, vp]
+        lib.orc_win_forward.restype = ctypes.c_int
+        lib.orc_win_backward.argtypes = [W, vp, vp, vp, vp, vp, vp, vp]
+        lib.orc_win_backward.restype = ctypes.c_int
         lib.orc_dwconv_forward.argtypes = [ctypes.POINTER(_Conv), vp, vp, vp, ctypes.c_int64,
                                            ctypes.c_int64, vp]
         lib.orc_dwconv_forward.restype = ctypes.c_int
@@ -300,4 +313,43 @@ def dwconv_backward(shape, dtype, x, w, dy, frames=None, weight_grads=True):
     if rc != 0:
         raise ValueError("oracle dwconv backward: malformed problem")
     return dx, dw, db
+
+
+# ----------------------------------------------------------------------------- window attention
+
+def _win(shape, dtype, scale):
+    B, T, H, W, heads, D, wt, wh, ww, st, sh, sw = shape
+    if scale is None:
+        scale = default_scale(D)
+    return _Win(B, T, H, W, heads, D, wt, wh, ww, st, sh, sw, float(scale),
+                1 if dtype == "bf16" else 0, 0)
+
+
+def win_forward(shape, dtype, q, k, v, frames=None, scale=None):
+    """Shifted-window attention output [B, t1-t0, H, W, heads, D] and LSE [B, t1-t0, H, W, heads]
+    (fp64) for frames [t0, t1) (all if None).  shape = (B, T, H, W, heads, D, wt, wh, ww,
+    st, sh, sw)."""
+    pr = _win(shape, dtype, scale)
+    q, k, v = (_check_io(a, dtype) for a in (q, k, v))
+    B, T, H, W, heads, D = shape[:6]
+    t0, t1 = (0, T) if frames is None else frames
+    out = np.empty((B, t1 - t0, H, W, heads, D), dtype=np.float64)
+    lse = np.empty((B, t1 - t0, H, W, heads), dtype=np.float64)
+    rc = _load().orc_win_forward(ctypes.byref(pr), q.ctypes.data, k.ctypes.data, v.ctypes.data,
+                                 t0, t1, out.ctypes.data, lse.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle window forward: malformed problem")
+    return out, lse
+
+
+def win_backward(shape, dtype, q, k, v, dout, scale=None):
+    """(dq, dk, dv) of the shifted-window attention, [B, T, H, W, heads, D] fp64."""
+    pr = _win(shape, dtype, scale)
+    q, k, v, dout = (_check_io(a, dtype) for a in (q, k, v, dout))
+    dq, dk, dv = (np.empty(q.shape, dtype=np.float64) for _ in range(3))
+    rc = _load().orc_win_backward(ctypes.byref(pr), q.ctypes.data, k.ctypes.data, v.ctypes.data,
+                                  dout.ctypes.data, dq.ctypes.data, dk.ctypes.data, dv.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle window backward: malformed problem")
+    return dq, dk, dv
 
