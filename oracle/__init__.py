@@ -79,7 +79,8 @@ def _load():
         W = ctypes.POINTER(_Win)
         lib.orc_win_forward.argtypes = [W, vp, vp, vp, ctypes.c_int64, ctypes.c_int64, vp, vp]
         lib.orc_win_forward.restype = ctypes.c_int
-        lib.orc_win_backward.argtypes = [W, vp, vp, vp, vp, vp, vp, vp]
+        lib.orc_win_backward.argtypes = [W, vp, vp, vp, vp, ctypes.c_int64, ctypes.c_int64, vp, vp,
+                                         vp]
         lib.orc_win_backward.restype = ctypes.c_int
         lib.orc_dwconv_forward.argtypes = [ctypes.POINTER(_Conv), vp, vp, vp, ctypes.c_int64,
                                            ctypes.c_int64, vp]
@@ -342,13 +343,18 @@ def win_forward(shape, dtype, q, k, v, frames=None, scale=None):
     return out, lse
 
 
-def win_backward(shape, dtype, q, k, v, dout, scale=None):
-    """(dq, dk, dv) of the shifted-window attention, [B, T, H, W, heads, D] fp64."""
+def win_backward(shape, dtype, q, k, v, dout, scale=None, frames=None):
+    """(dq, dk, dv) of the shifted-window attention for the tokens of frames [t0, t1) (all if
+    None), [B, t1 - t0, H, W, heads, D] fp64: dq is complete, dk and dv hold the contributions
+    of the queries in the range (complete for keys whose window region lies inside it)."""
     pr = _win(shape, dtype, scale)
     q, k, v, dout = (_check_io(a, dtype) for a in (q, k, v, dout))
-    dq, dk, dv = (np.empty(q.shape, dtype=np.float64) for _ in range(3))
+    t0, t1 = (0, shape[1]) if frames is None else frames
+    oshape = (q.shape[0], t1 - t0) + tuple(q.shape[2:])
+    dq, dk, dv = (np.empty(oshape, dtype=np.float64) for _ in range(3))
     rc = _load().orc_win_backward(ctypes.byref(pr), q.ctypes.data, k.ctypes.data, v.ctypes.data,
-                                  dout.ctypes.data, dq.ctypes.data, dk.ctypes.data, dv.ctypes.data)
+                                  dout.ctypes.data, t0, t1, dq.ctypes.data, dk.ctypes.data,
+                                  dv.ctypes.data)
     if rc != 0:
         raise ValueError("oracle window backward: malformed problem")
     return dq, dk, dv

@@ -130,12 +130,17 @@ int orc_win_forward(const orc_win* p, const void* q, const void* k, const void* 
   return 0;
 }
 
-/* Full backward: dq, dk, dv [B][T][H][W][heads][D] (overwritten), fp64. */
+/* Backward over the queries of frames [t0, t1): dq, dk, dv [B][t1 - t0][H][W][heads][D]
+ * (overwritten, fp64) for the tokens of those frames.  dq is complete; dk and dv receive the
+ * contributions of the queries in the range, so they are complete for keys whose window
+ * region lies inside the range (all of them for the full range). */
 int orc_win_backward(const orc_win* p, const void* q, const void* k, const void* v,
-                     const void* dout, double* dq, double* dk, double* dv) {
-  if (wa_bad(p)) return 1;
+                     const void* dout, int64_t t0, int64_t t1, double* dq, double* dk,
+                     double* dv) {
+  if (wa_bad(p) || t0 < 0 || t1 > p->T || t0 > t1) return 1;
   const int64_t N = p->T * p->H * p->W, D = p->D, M = p->heads, nw = p->wt * p->wh * p->ww;
-  const int64_t total = p->B * N * M * D;
+  const int64_t HW = p->H * p->W, NR = (t1 - t0) * HW; /* tokens per batch item in the range */
+  const int64_t total = p->B * NR * M * D;
   memset(dq, 0, sizeof(double) * total);
   memset(dk, 0, sizeof(double) * total);
   memset(dv, 0, sizeof(double) * total);
@@ -146,7 +151,7 @@ int orc_win_backward(const orc_win* p, const void* q, const void* k, const void*
     double* dp = (double*)malloc(sizeof(double) * nw);
 #pragma omp for collapse(2) schedule(dynamic, 16)
     for (int64_t b = 0; b < p->B; ++b)
-      for (int64_t n = 0; n < N; ++n) {
+      for (int64_t n = t0 * p->H * p->W; n < t1 * p->H * p->W; ++n) {
         const int64_t t = n / (p->H * p->W), i = (n / p->W) % p->H, j = n % p->W;
         const int64_t nk = wa_keys(p, t, i, j, keys);
         for (int64_t m = 0; m < M; ++m) {
@@ -167,18 +172,22 @@ int orc_win_backward(const orc_win* p, const void* q, const void* k, const void*
           for (int64_t c = 0; c < nk; ++c) l += exp(s[c] - mx);
           double delta = 0.0;
           for (int64_t c = 0; c < nk; ++c) delta += exp(s[c] - mx) / l * dp[c];
+          const int64_t orow = ((b * NR + n - t0 * HW) * M + m) * D; /* this query's output row */
           for (int64_t c = 0; c < nk; ++c) {
             const double al = exp(s[c] - mx) / l;
             const double ds = al * (dp[c] - delta);
             const int64_t krow = ((b * N + keys[c]) * M + m) * D;
+            const int64_t kt = keys[c] / HW;
+            const int64_t okrow = ((b * NR + keys[c] - t0 * HW) * M + m) * D;
             for (int64_t d = 0; d < D; ++d) {
-              dq[qrow + d] += p->scale * ds * wa_ld(k, p->bf16, krow + d);
+              dq[orow + d] += p->scale * ds * wa_ld(k, p->bf16, krow + d);
+              if (kt < t0 || kt >= t1) continue;
               const double addk = p->scale * ds * wa_ld(q, p->bf16, qrow + d);
               const double addv = al * wa_ld(dout, p->bf16, qrow + d);
 #pragma omp atomic
-              dk[krow + d] += addk;
+              dk[okrow + d] += addk;
 #pragma omp atomic
-              dv[krow + d] += addv;
+              dv[okrow + d] += addv;
             }
           }
         }

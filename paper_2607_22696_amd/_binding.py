@@ -34,7 +34,11 @@ EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_timed",
             "dsa3d_backward_workspace_size", "dsa3d_status_string", "dsa3d_abi_version",
             "dsa3d_dwconv3d_forward", "dsa3d_dwconv3d_backward_workspace_size",
             "dsa3d_dwconv3d_backward", "dsa3d_pw_forward", "dsa3d_pw_backward_workspace_size",
-            "dsa3d_pw_backward")
+            "dsa3d_pw_backward", "dsa3d_win_forward", "dsa3d_win_backward_workspace_size",
+            "dsa3d_win_backward")
+
+DSA3D_WIN_MAX_TOKENS = 65536
+DSA3D_WIN_BACKWARD_PHASES = 2
 
 
 class dsa3d_desc(ctypes.Structure):
@@ -48,6 +52,14 @@ class dsa3d_dwconv_desc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("frames", ctypes.c_int32), ("height", ctypes.c_int32),
                 ("width", ctypes.c_int32), ("channels", ctypes.c_int32), ("kt", ctypes.c_int32),
                 ("kh", ctypes.c_int32), ("kw", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class dsa3d_win_desc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("frames", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("wt", ctypes.c_int32), ("wh", ctypes.c_int32), ("ww", ctypes.c_int32),
+                ("st", ctypes.c_int32), ("sh", ctypes.c_int32), ("sw", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
 
 
 class Dsa3dError(RuntimeError):
@@ -91,6 +103,14 @@ def load():
         lib.dsa3d_dwconv3d_backward.argtypes = [cd, vp, vp, vp, vp, ctypes.c_int, vp, vp, vp,
                                                 ctypes.c_size_t, vp]
         lib.dsa3d_dwconv3d_backward.restype = ctypes.c_int
+        wd = ctypes.POINTER(dsa3d_win_desc)
+        lib.dsa3d_win_forward.argtypes = [wd, vp, vp, vp, vp, vp, vp, vp]
+        lib.dsa3d_win_forward.restype = ctypes.c_int
+        lib.dsa3d_win_backward_workspace_size.argtypes = [wd]
+        lib.dsa3d_win_backward_workspace_size.restype = ctypes.c_size_t
+        lib.dsa3d_win_backward.argtypes = [wd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                           ctypes.c_size_t, vp, ctypes.POINTER(vp)]
+        lib.dsa3d_win_backward.restype = ctypes.c_int
         lib.dsa3d_backward_workspace_size.argtypes = [pd]
         lib.dsa3d_backward_workspace_size.restype = ctypes.c_size_t
         lib.dsa3d_status_string.argtypes = [ctypes.c_int]
@@ -182,13 +202,13 @@ def dsa3d_pw_backward_workspace_size(desc) -> int:
     return load().dsa3d_pw_backward_workspace_size(ctypes.byref(desc))
 
 
-def _event_array(events):
-    """None, or a ctypes array of DSA3D_BACKWARD_PHASES + 1 created event handles."""
+def _event_array(events, phases=DSA3D_BACKWARD_PHASES):
+    """None, or a ctypes array of phases + 1 created event handles."""
     if events is None:
         return None
     handles = [e if isinstance(e, int) else e.cuda_event for e in events]
-    if len(handles) != DSA3D_BACKWARD_PHASES + 1 or not all(handles):
-        raise ValueError("phase timing needs DSA3D_BACKWARD_PHASES + 1 created events")
+    if len(handles) != phases + 1 or not all(handles):
+        raise ValueError(f"phase timing needs {phases} + 1 created events")
     return (ctypes.c_void_p * len(handles))(*handles)
 
 
@@ -231,6 +251,39 @@ def dsa3d_dwconv3d_backward(desc, x, weight, dy, dx, dweight, dbias, workspace=N
                                         _ptr(workspace), workspace_bytes, _stream(stream))
     if check and st != DSA3D_OK:
         raise Dsa3dError(st, "dsa3d_dwconv3d_backward")
+    return st
+
+
+def make_win_desc(B, T, H, W, heads, head_dim, window, shift=(0, 0, 0), dtype="bf16",
+                  scale=0.0) -> dsa3d_win_desc:
+    return dsa3d_win_desc(B, T, H, W, heads, head_dim, *window, *shift, float(scale),
+                          DSA3D_BF16 if dtype == "bf16" else DSA3D_F32)
+
+
+def dsa3d_win_forward(desc, q, k, v, out, out_res=None, lse=None, stream=None,
+                      check=True) -> int:
+    st = load().dsa3d_win_forward(ctypes.byref(desc) if desc is not None else None, _ptr(q),
+                                  _ptr(k), _ptr(v), _ptr(out), _ptr(out_res), _ptr(lse),
+                                  _stream(stream))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_win_forward")
+    return st
+
+
+def dsa3d_win_backward_workspace_size(desc) -> int:
+    return load().dsa3d_win_backward_workspace_size(ctypes.byref(desc))
+
+
+def dsa3d_win_backward(desc, q, k, v, out, out_res, lse, dout, dq, dk, dv, workspace=None,
+                       workspace_bytes=0, stream=None, events=None, check=True) -> int:
+    st = load().dsa3d_win_backward(ctypes.byref(desc) if desc is not None else None, _ptr(q),
+                                   _ptr(k), _ptr(v), _ptr(out), _ptr(out_res), _ptr(lse),
+                                   _ptr(dout), _ptr(dq),
+                                   _ptr(dk), _ptr(dv), _ptr(workspace), workspace_bytes,
+                                   _stream(stream),
+                                   _event_array(events, DSA3D_WIN_BACKWARD_PHASES))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_win_backward")
     return st
 
 

@@ -60,4 +60,32 @@ hipError_t launch_conv_backward(const ConvGeometry& g, bool bf16, const void* x,
                                 const void* dy, float* dx, int accumulate_dx, float* dw, float* db,
                                 void* workspace, hipStream_t stream);
 
+// ---------------------------------------------------------------------------- window attention
+
+// Shifted-window attention geometry (validated on the host; filled by win_plan).  Along each
+// axis the cut points of the box partition are off + n * window (off = shift - window for a
+// non-zero shift, else 0), clipped to the grid.
+struct WinGeometry {
+  int B, T, H, W, heads, D;
+  int wt, wh, ww;            // window
+  int off_t, off_h, off_w;   // first cut point minus one window
+  int nt, nh, nw, boxes;     // boxes per axis and in all
+  int max_box;               // largest box volume
+  int qtiles;                // query tiles of the largest box
+  int groups;                // (batch, box, head) groups, B * boxes * heads
+  int N;                     // tokens per batch item
+  float scale, scale_log2;   // logit scale (natural-log units) and scale * log2(e)
+};
+
+// Fills the cut points, box counts and launch sizes from B..D, the window and the shifts.
+void win_plan(WinGeometry& g, int st, int sh, int sw);
+int64_t win_forward_blocks(const WinGeometry& g);
+// out_res may be null (not written / not read).
+hipError_t launch_win_forward(const WinGeometry& g, const void* q, const void* k, const void* v,
+                              void* out, void* out_res, float* lse, hipStream_t stream);
+hipError_t launch_win_backward(const WinGeometry& g, const void* q, const void* k, const void* v,
+                               const void* out, const void* out_res, const float* lse,
+                               const void* dout, float* dq, float* dk, float* dv,
+                               void* workspace, hipStream_t stream, hipEvent_t const* events);
+
 }  // namespace dsa3d

@@ -1,0 +1,643 @@
+// Fixed / shifted 3D window attention (the Swin-DiT baseline of Section 6.2), gfx950 kernels.
+//
+// The shifted-window partition is handled as a partition of the grid into boxes: along each
+// axis the cut points are off + n * window, clipped to the grid, and every box attends densely
+// within itself (the keys a rolled window's mask keeps for a query are exactly the real tokens
+// of the query's box).  A workgroup takes one (batch, box, head) group and one tile of 128 of
+// its queries; the tiles of a group are given blocks of one XCD, so its K and V rows are
+// served from that XCD's L2 after the first read.
+//
+// Matrix products use v_mfma_f32_32x32x16_bf16.  For A (32 x 16), B (16 x 32) and C (32 x 32)
+// lane l holds row (of A) or column (of B) l % 32 with k = 8 (l / 32) .. +7, and C column
+// l % 32 with rows 8 (i / 4) + 4 (l / 32) + i % 4 in its element i.  The kernels compute the
+// transposed products (S^T = K Q^T, O^T = V^T P^T and so on) so that a lane owns one query's
+// (or key's) column: the softmax statistics then need only one exchange with lane l ^ 32, and
+// the logits in C layout are already the B operand of the next product once the keys are
+// taken in the order lane l's 8 registers hold them (the A operand, read from a transposed LDS
+// tile, uses the same order).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "dsa3d_internal.h"
+
+namespace dsa3d {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+constexpr int kQTile = 128;  // queries per workgroup: 4 waves x 32
+constexpr int kTile = 64;    // rows per LDS tile (keys of the forward and dq passes, queries
+                             // of the dk/dv pass)
+constexpr int kXcd = 8;
+constexpr float kLn2 = 0.6931471805599453f;
+
+struct Box {
+  int t0, i0, j0, lh, lw, n;
+  float inv_hw, inv_w;
+};
+
+__device__ inline void axis_cut(int a, int off, int win, int size, int& lo, int& len) {
+  const int s = off + a * win, e = s + win;
+  lo = s > 0 ? s : 0;
+  len = (e < size ? e : size) - lo;
+}
+
+__device__ inline Box box_of(const WinGeometry& g, int box) {
+  const int aw = box % g.nw, r = box / g.nw, ah = r % g.nh, at = r / g.nh;
+  Box bx;
+  int lt;
+  axis_cut(at, g.off_t, g.wt, g.T, bx.t0, lt);
+  axis_cut(ah, g.off_h, g.wh, g.H, bx.i0, bx.lh);
+  axis_cut(aw, g.off_w, g.ww, g.W, bx.j0, bx.lw);
+  bx.n = lt * bx.lh * bx.lw;
+  bx.inv_hw = 1.0f / (float)(bx.lh * bx.lw);
+  bx.inv_w = 1.0f / (float)bx.lw;
+  return bx;
+}
+
+// Token (t * H + i) * W + j of box-local index u, box-major (t, then i, then j).  u is below
+// 2^16, so the float quotients (u + 1/2) / d, whose distance to an integer is at least 1/(2d),
+// are floored exactly.
+__device__ inline int box_token(const WinGeometry& g, const Box& bx, int u) {
+  const int a = (int)(((float)u + 0.5f) * bx.inv_hw);
+  const int rem = u - a * bx.lh * bx.lw;
+  const int e = (int)(((float)rem + 0.5f) * bx.inv_w);
+  return ((bx.t0 + a) * g.H + bx.i0 + e) * g.W + bx.j0 + (rem - e * bx.lw);
+}
+
+struct Group {
+  int b, m, qt;
+  Box bx;
+};
+
+// Block -> (batch, box, head) group and query tile.  Dispatch hands block x to XCD x % 8, so
+// the tiles of a group are given blocks congruent modulo 8.  Returns false for padding blocks.
+__device__ inline bool group_of(const WinGeometry& g, int tiles, Group& gr) {
+  const int x = blockIdx.x % kXcd, r = blockIdx.x / kXcd;
+  gr.qt = r % tiles;
+  const int grp = (r / tiles) * kXcd + x;
+  if (grp >= g.groups) return false;
+  gr.m = grp % g.heads;
+  const int r2 = grp / g.heads;
+  gr.b = r2 / g.boxes;
+  gr.bx = box_of(g, r2 % g.boxes);
+  return true;
+}
+
+__device__ inline int64_t row_of(const WinGeometry& g, int b, int tok, int m) {
+  return ((int64_t)b * g.N + tok) * g.heads + m;
+}
+
+__device__ inline f32x16_t mfma(const bf16x8_t& a, const bf16x8_t& b, const f32x16_t& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ inline bf16x8_t as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
+
+// Two bf16 of one column of a row pair: keys k0 (low half of the result) and k1.
+__device__ inline uint32_t pick_pair(uint32_t k1, uint32_t k0, bool high) {
+  return __builtin_amdgcn_perm(k1, k0, high ? 0x07060302u : 0x05040100u);
+}
+
+// Staging of a tile of kTile box rows (box-local indices base .. base + kTile - 1; rows past the
+// box end read as zero) of a [rows][D] bf16 tensor into LDS, gathered through the box's token
+// order.  Row-major tiles keep rows of D channels (pitch D + 8: 16-byte reads of 8 lanes on 8
+// consecutive rows hit distinct banks); transposed tiles keep, per channel, the kTile rows
+// (pitch kTile + 4).  Each thread moves NL 16-byte chunks.
+template <int D>
+struct Tile {
+  static constexpr int RP = D + 8;                   // row-major pitch (bf16)
+  static constexpr int TP = kTile + 4;               // transposed pitch (bf16)
+  static constexpr int KCH = D / 8;                  // 16-byte chunks per row
+  static constexpr int NL = kTile * KCH / kThreads;  // chunks per thread
+  static constexpr int VG = kTile / NL;              // row groups of the transposed staging
+  static constexpr int kRowElems = kTile * RP;
+  static constexpr int kColElems = D * TP;
+  static_assert(NL == 2 || NL == 4, "head_dim 64 or 128");
+
+  // Row-major: thread t moves chunk t % KCH of rows t / KCH + r * (kThreads / KCH).
+  static __device__ inline void load_rows(uint4 (&r)[NL], const uint16_t* src, const WinGeometry& g,
+                                          const Group& gr, int base) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int u = base + t / KCH + i * (kThreads / KCH);
+      r[i] = make_uint4(0, 0, 0, 0);
+      if (u < gr.bx.n)
+        r[i] = *reinterpret_cast<const uint4*>(
+            src + row_of(g, gr.b, box_token(g, gr.bx, u), gr.m) * D + (t % KCH) * 8);
+    }
+  }
+  static __device__ inline void store_rows(uint16_t* lds, const uint4 (&r)[NL]) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < NL; ++i)
+      *reinterpret_cast<uint4*>(lds + (t / KCH + i * (kThreads / KCH)) * RP + (t % KCH) * 8) = r[i];
+  }
+
+  // Transposed: thread t moves chunk t / VG of rows (t % VG) * NL + e, e < NL, and writes, for
+  // each of the chunk's 8 channels, its NL rows as one 4- or 8-byte word.
+  static __device__ inline void load_cols(uint4 (&r)[NL], const uint16_t* src, const WinGeometry& g,
+                                          const Group& gr, int base) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int e = 0; e < NL; ++e) {
+      const int u = base + (t % VG) * NL + e;
+      r[e] = make_uint4(0, 0, 0, 0);
+      if (u < gr.bx.n)
+        r[e] = *reinterpret_cast<const uint4*>(
+            src + row_of(g, gr.b, box_token(g, gr.bx, u), gr.m) * D + (t / VG) * 8);
+    }
+  }
+  static __device__ inline void store_cols(uint16_t* lds, const uint4 (&r)[NL]) {
+    const int t = threadIdx.x, kg = t % VG, c = t / VG;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const bool hi = x & 1;
+      const int w = x >> 1;
+      uint16_t* dst = lds + (c * 8 + x) * TP + kg * NL;
+      const uint32_t w0 = pick_pair(word(r[1], w), word(r[0], w), hi);
+      if constexpr (NL == 4) {
+        const uint32_t w1 = pick_pair(word(r[3], w), word(r[2], w), hi);
+        *reinterpret_cast<uint2*>(dst) = make_uint2(w0, w1);
+      } else {
+        *reinterpret_cast<uint32_t*>(dst) = w0;
+      }
+    }
+  }
+
+  // A operand from a row-major tile: row r0 + l % 32, channels 16 ks + 8 (l / 32) .. +7.
+  static __device__ inline bf16x8_t a_rows(const uint16_t* lds, int r0, int ks) {
+    const int lane = threadIdx.x & 63;
+    return as_bf16x8(*reinterpret_cast<const uint4*>(lds + (r0 + (lane & 31)) * RP + ks * 16 +
+                                                     (lane >> 5) * 8));
+  }
+  // A operand from a transposed tile: channel d0 + l % 32; tile rows 32 kb + 16 p + 4 (l / 32)
+  // + {0..3, 8..11}, the order in which a C-layout block's elements 8 p .. 8 p + 7 hold them.
+  static __device__ inline bf16x8_t a_cols(const uint16_t* lds, int d0, int kb, int p) {
+    const int lane = threadIdx.x & 63;
+    const uint16_t* src = lds + (d0 + (lane & 31)) * TP + kb * 32 + 16 * p + 4 * (lane >> 5);
+    const uint2 lo = *reinterpret_cast<const uint2*>(src);
+    const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
+    return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+  }
+
+  static __device__ inline uint32_t word(const uint4& u, int w) {
+    return w == 0 ? u.x : (w == 1 ? u.y : (w == 2 ? u.z : u.w));
+  }
+};
+
+// Fragment of this lane's row as the B operand: channels 16 ks + 8 (l / 32) .. +7 (zero for a
+// row past the box end).
+template <int D>
+__device__ inline void load_frag(bf16x8_t (&f)[D / 16], const uint16_t* src, int64_t row, bool ok) {
+  const int hh = (threadIdx.x & 63) >> 5;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    uint4 u = make_uint4(0, 0, 0, 0);
+    if (ok) u = *reinterpret_cast<const uint4*>(src + row * D + ks * 16 + hh * 8);
+    f[ks] = as_bf16x8(u);
+  }
+}
+
+// Sixteen C-layout values as B-operand fragments (elements 8 p .. 8 p + 7) of a bf16 pair
+// hi + lo: hi = bf16(x), lo = bf16(x - hi).  The pair carries about 16 significant bits, so a
+// product taken as two MFMAs (hi and lo) loses almost nothing to the bf16 operand.
+__device__ inline void to_frags(const float (&x)[16], bf16x8_t (&hi)[2], bf16x8_t (&lo)[2]) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const __bf16 h = (__bf16)x[i];
+    hi[i / 8][i % 8] = h;
+    lo[i / 8][i % 8] = (__bf16)(x[i] - (float)h);
+  }
+}
+
+// Stores this lane's 16 fp32 C-layout values of channel block db (channels 32 db + 8 blk +
+// 4 (l / 32) + j) times `mul` to a float row.
+__device__ inline void store_f32_block(float* row, int db, const f32x16_t& acc, float mul) {
+  const int hh = (threadIdx.x & 63) >> 5;
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk)
+    *reinterpret_cast<float4*>(row + db * 32 + 8 * blk + 4 * hh) =
+        make_float4(acc[4 * blk] * mul, acc[4 * blk + 1] * mul, acc[4 * blk + 2] * mul,
+                    acc[4 * blk + 3] * mul);
+}
+
+// ---------------------------------------------------------------------------- forward
+
+// Online-softmax state of one query (lanes l and l ^ 32 keep identical copies): running
+// maximum of the base-2 logits and the partial sum over this lane's half of the keys.
+struct Softmax {
+  float m = -INFINITY, l = 0.0f;
+};
+
+// One workgroup: 128 queries of one (batch, box, head) group against every key of the box,
+// 64 keys per LDS tile, online base-2 softmax.  Wave w owns queries 32 w .. 32 w + 31 of the
+// tile; lanes l and l ^ 32 share query l % 32 and hold 16 of each 32-key block's logits each.
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void
+win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+               const uint16_t* __restrict__ v, uint16_t* __restrict__ out,
+               uint16_t* __restrict__ out_res, float* __restrict__ lse) {
+  using Tl = Tile<D>;
+  constexpr int KS = D / 16;  // MFMA k-steps over head_dim
+  constexpr int DB = D / 32;  // 32-channel blocks of the output
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kRowElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[Tl::kColElems];
+
+  Group gr;
+  if (!group_of(g, g.qtiles, gr)) return;
+  const int q0 = gr.qt * kQTile, n = gr.bx.n;
+  if (q0 >= n) return;  // the box has fewer tiles than the largest one
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
+  const int uq = q0 + wave * 32 + (lane & 31);
+  const bool qok = uq < n;
+  const int64_t qrow = qok ? row_of(g, gr.b, box_token(g, gr.bx, uq), gr.m) : 0;
+  bf16x8_t qf[KS];  // Q^T as the B operand
+  load_frag<D>(qf, q, qrow, qok);
+
+  f32x16_t o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[db] = f32x16_t{};
+  Softmax sm;
+
+  uint4 kr[Tl::NL], vr[Tl::NL];
+  const int ntiles = (n + kTile - 1) / kTile;
+  Tl::load_rows(kr, k, g, gr, 0);
+  Tl::load_cols(vr, v, g, gr, 0);
+  for (int kt = 0; kt < ntiles; ++kt) {
+    Tl::store_rows(Ks, kr);
+    Tl::store_cols(Vt, vr);
+    __syncthreads();
+    if (kt + 1 < ntiles) {
+      Tl::load_rows(kr, k, g, gr, (kt + 1) * kTile);
+      Tl::load_cols(vr, v, g, gr, (kt + 1) * kTile);
+    }
+
+    // S^T = K Q^T for the two 32-key blocks of the tile
+    float s[2][16];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16_t acc = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) acc = mfma(Tl::a_rows(Ks, kb * 32, ks), qf[ks], acc);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s[kb][i] = acc[i];
+    }
+    const int kbase = kt * kTile;
+    if (kbase + kTile > n) {  // ragged last tile: keys past the box end get -inf
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (kbase + kb * 32 + 8 * (i / 4) + 4 * hh + (i % 4) >= n) s[kb][i] = -INFINITY;
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(sm.m, mx * g.scale_log2);  // scale > 0
+    const float corr = __builtin_amdgcn_exp2f(sm.m - mnew);
+    sm.m = mnew;
+    sm.l *= corr;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] *= corr;
+
+    bf16x8_t ph[2][2], pl[2][2];  // P^T as B-operand fragments (hi + lo)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        s[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[kb][i], g.scale_log2, -mnew));
+        sm.l += s[kb][i];
+      }
+      to_frags(s[kb], ph[kb], pl[kb]);
+    }
+
+    // O^T += V^T P^T
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const bf16x8_t a = Tl::a_cols(Vt, db * 32, kb, p);
+          o[db] = mfma(a, ph[kb][p], o[db]);
+          o[db] = mfma(a, pl[kb][p], o[db]);
+        }
+    __syncthreads();
+  }
+
+  const float ltot = sm.l + __shfl_xor(sm.l, 32);
+  if (!qok) return;
+  const float inv = 1.0f / ltot;
+  const int64_t obase = qrow * D + 4 * hh;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+      __bf16 h[4], r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float x = o[db][4 * blk + j] * inv;
+        h[j] = (__bf16)x;
+        r[j] = (__bf16)(x - (float)h[j]);
+      }
+      const int64_t at = obase + db * 32 + 8 * blk;
+      *reinterpret_cast<uint2*>(out + at) = __builtin_bit_cast(uint2, h);
+      if (out_res != nullptr) *reinterpret_cast<uint2*>(out_res + at) = __builtin_bit_cast(uint2, r);
+    }
+  if (hh == 0 && lse != nullptr) lse[qrow] = (sm.m + __builtin_amdgcn_logf(ltot)) * kLn2;
+}
+
+// ---------------------------------------------------------------------------- backward
+
+// dq pass: 128 queries of one group against every key of the box (as the forward), with
+//   P = exp2(s log2(e) scale - lse log2(e)),  dP^T = V dout^T,  dS = P (dP - Delta),
+//   dq^T += K^T dS^T  (scaled by `scale` at the end),
+// and Delta = <dout, out + out_res> of each query (out alone without the residual), written
+// to `delta` for the dk/dv pass.
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void
+win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+              const uint16_t* __restrict__ v, const uint16_t* __restrict__ out,
+              const uint16_t* __restrict__ out_res, const float* __restrict__ lse,
+              const uint16_t* __restrict__ dout, float* __restrict__ dq,
+              float* __restrict__ delta) {
+  using Tl = Tile<D>;
+  constexpr int KS = D / 16, DB = D / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kRowElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[Tl::kRowElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Kt[Tl::kColElems];
+
+  Group gr;
+  if (!group_of(g, g.qtiles, gr)) return;
+  const int q0 = gr.qt * kQTile, n = gr.bx.n;
+  if (q0 >= n) return;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
+  const int uq = q0 + wave * 32 + (lane & 31);
+  const bool qok = uq < n;
+  const int64_t qrow = qok ? row_of(g, gr.b, box_token(g, gr.bx, uq), gr.m) : 0;
+  bf16x8_t qf[KS], gf[KS];
+  load_frag<D>(qf, q, qrow, qok);
+  load_frag<D>(gf, dout, qrow, qok);
+  float dl;
+  {
+    bf16x8_t of[KS], rf[KS];
+    load_frag<D>(of, out, qrow, qok);
+    load_frag<D>(rf, out_res, qrow, qok && out_res != nullptr);
+    float part = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        part = fmaf((float)gf[ks][e], (float)of[ks][e] + (float)rf[ks][e], part);
+    dl = part + __shfl_xor(part, 32);
+  }
+  if (qok && hh == 0) delta[qrow] = dl;
+  const float lse2 = qok ? lse[qrow] * 1.4426950408889634f : 0.0f;
+
+  f32x16_t acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16_t{};
+
+  uint4 kr[Tl::NL], vr[Tl::NL], kc[Tl::NL];
+  const int ntiles = (n + kTile - 1) / kTile;
+  Tl::load_rows(kr, k, g, gr, 0);
+  Tl::load_rows(vr, v, g, gr, 0);
+  Tl::load_cols(kc, k, g, gr, 0);
+  for (int kt = 0; kt < ntiles; ++kt) {
+    Tl::store_rows(Ks, kr);
+    Tl::store_rows(Vs, vr);
+    Tl::store_cols(Kt, kc);
+    __syncthreads();
+    if (kt + 1 < ntiles) {
+      Tl::load_rows(kr, k, g, gr, (kt + 1) * kTile);
+      Tl::load_rows(vr, v, g, gr, (kt + 1) * kTile);
+      Tl::load_cols(kc, k, g, gr, (kt + 1) * kTile);
+    }
+    const int kbase = kt * kTile;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16_t sa = f32x16_t{}, pa = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        sa = mfma(Tl::a_rows(Ks, kb * 32, ks), qf[ks], sa);
+        pa = mfma(Tl::a_rows(Vs, kb * 32, ks), gf[ks], pa);
+      }
+      float ds[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const bool ok = kbase + kb * 32 + 8 * (i / 4) + 4 * hh + (i % 4) < n;
+        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(sa[i], g.scale_log2, -lse2)) : 0.0f;
+        ds[i] = p * (pa[i] - dl);
+      }
+      bf16x8_t dh[2], dlo[2];
+      to_frags(ds, dh, dlo);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const bf16x8_t a = Tl::a_cols(Kt, db * 32, kb, p);
+          acc[db] = mfma(a, dh[p], acc[db]);
+          acc[db] = mfma(a, dlo[p], acc[db]);
+        }
+    }
+    __syncthreads();
+  }
+  if (!qok) return;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) store_f32_block(dq + qrow * D, db, acc[db], g.scale);
+}
+
+// dk/dv pass: 128 keys of one group (wave w owns keys 32 w .. 32 w + 31, lanes l and l ^ 32
+// share key l % 32) against every query of the box, 64 queries per LDS tile:
+//   S = Q K^T,  P = exp2(s log2(e) scale - lse log2(e)),  dP = dout V^T,  dS = P (dP - Delta),
+//   dv^T += dout^T P,  dk^T += Q^T dS  (scaled by `scale` at the end).
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(D == 128 ? 1 : 2, 2))) void
+win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                const uint16_t* __restrict__ v, const float* __restrict__ lse,
+                const uint16_t* __restrict__ dout, const float* __restrict__ delta,
+                float* __restrict__ dk, float* __restrict__ dv) {
+  using Tl = Tile<D>;
+  constexpr int KS = D / 16, DB = D / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[Tl::kRowElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Gs[Tl::kRowElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Qt[Tl::kColElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Gt[Tl::kColElems];
+  __shared__ __attribute__((aligned(16))) float Ls[kTile];  // lse log2(e); +inf past the box end
+  __shared__ __attribute__((aligned(16))) float Dl[kTile];  // Delta
+
+  Group gr;
+  if (!group_of(g, g.qtiles, gr)) return;
+  const int k0 = gr.qt * kQTile, n = gr.bx.n;
+  if (k0 >= n) return;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
+  const int uk = k0 + wave * 32 + (lane & 31);
+  const bool kok = uk < n;
+  const int64_t krow = kok ? row_of(g, gr.b, box_token(g, gr.bx, uk), gr.m) : 0;
+  bf16x8_t kf[KS], vf[KS];  // K^T and V^T as B operands
+  load_frag<D>(kf, k, krow, kok);
+  load_frag<D>(vf, v, krow, kok);
+
+  f32x16_t dka[DB], dva[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) dka[db] = dva[db] = f32x16_t{};
+
+  const int ntiles = (n + kTile - 1) / kTile;
+  for (int qt = 0; qt < ntiles; ++qt) {
+    const int qbase = qt * kTile;
+    {
+      uint4 r[Tl::NL];
+      Tl::load_rows(r, q, g, gr, qbase);
+      Tl::store_rows(Qs, r);
+      Tl::load_cols(r, q, g, gr, qbase);
+      Tl::store_cols(Qt, r);
+      Tl::load_rows(r, dout, g, gr, qbase);
+      Tl::store_rows(Gs, r);
+      Tl::load_cols(r, dout, g, gr, qbase);
+      Tl::store_cols(Gt, r);
+      if (threadIdx.x < kTile) {
+        const int u = qbase + threadIdx.x;
+        float ls = INFINITY, de = 0.0f;
+        if (u < n) {
+          const int64_t row = row_of(g, gr.b, box_token(g, gr.bx, u), gr.m);
+          ls = lse[row] * 1.4426950408889634f;
+          de = delta[row];
+        }
+        Ls[threadIdx.x] = ls;
+        Dl[threadIdx.x] = de;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      f32x16_t sa = f32x16_t{}, pa = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        sa = mfma(Tl::a_rows(Qs, qb * 32, ks), kf[ks], sa);
+        pa = mfma(Tl::a_rows(Gs, qb * 32, ks), vf[ks], pa);
+      }
+      float p[16], ds[16];
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) {
+        const float4 l4 = *reinterpret_cast<const float4*>(Ls + qb * 32 + 8 * blk + 4 * hh);
+        const float4 d4 = *reinterpret_cast<const float4*>(Dl + qb * 32 + 8 * blk + 4 * hh);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int i = 4 * blk + j;
+          p[i] = __builtin_amdgcn_exp2f(fmaf(sa[i], g.scale_log2, -lv[j]));
+          ds[i] = p[i] * (pa[i] - dv4[j]);
+        }
+      }
+      bf16x8_t ph[2], pl[2], dh[2], dlo[2];
+      to_frags(p, ph, pl);
+      to_frags(ds, dh, dlo);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+          const bf16x8_t ag = Tl::a_cols(Gt, db * 32, qb, pp);
+          dva[db] = mfma(ag, ph[pp], dva[db]);
+          dva[db] = mfma(ag, pl[pp], dva[db]);
+          const bf16x8_t aq = Tl::a_cols(Qt, db * 32, qb, pp);
+          dka[db] = mfma(aq, dh[pp], dka[db]);
+          dka[db] = mfma(aq, dlo[pp], dka[db]);
+        }
+    }
+    __syncthreads();
+  }
+  if (!kok) return;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    store_f32_block(dk + krow * D, db, dka[db], g.scale);
+    store_f32_block(dv + krow * D, db, dva[db], 1.0f);
+  }
+}
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+hipError_t mark(hipEvent_t const* events, int i, hipStream_t s) {
+  return events != nullptr ? hipEventRecord(events[i], s) : hipSuccess;
+}
+
+template <int D>
+hipError_t win_backward_d(const WinGeometry& g, const uint16_t* q, const uint16_t* k,
+                          const uint16_t* v, const uint16_t* out, const uint16_t* res,
+                          const float* lse,
+                          const uint16_t* dout, float* dq, float* dk, float* dv, float* delta,
+                          hipStream_t s, hipEvent_t const* events) {
+  const dim3 grid((unsigned)win_forward_blocks(g)), block(kThreads);
+  void* a1[] = {(void*)&g,   (void*)&q,    (void*)&k,  (void*)&v,    (void*)&out,
+                (void*)&res, (void*)&lse, (void*)&dout, (void*)&dq, (void*)&delta};
+  hipError_t e = mark(events, 0, s);
+  if (e == hipSuccess)
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&win_dq_kernel<D>), grid, block, a1, 0, s);
+  if (e == hipSuccess) e = mark(events, 1, s);
+  if (e != hipSuccess) return e;
+  const float* cdelta = delta;
+  void* a2[] = {(void*)&g,   (void*)&q,    (void*)&k,      (void*)&v, (void*)&lse,
+                (void*)&dout, (void*)&cdelta, (void*)&dk, (void*)&dv};
+  e = hipLaunchKernel(reinterpret_cast<const void*>(&win_dkdv_kernel<D>), grid, block, a2, 0, s);
+  return e == hipSuccess ? mark(events, 2, s) : e;
+}
+
+}  // namespace
+
+void win_plan(WinGeometry& g, int st, int sh, int sw) {
+  g.off_t = st > 0 ? st - g.wt : 0;
+  g.off_h = sh > 0 ? sh - g.wh : 0;
+  g.off_w = sw > 0 ? sw - g.ww : 0;
+  g.nt = ceil_div(g.T - g.off_t, g.wt);
+  g.nh = ceil_div(g.H - g.off_h, g.wh);
+  g.nw = ceil_div(g.W - g.off_w, g.ww);
+  g.boxes = g.nt * g.nh * g.nw;
+  g.max_box = std::min(g.wt, g.T) * std::min(g.wh, g.H) * std::min(g.ww, g.W);
+  g.qtiles = ceil_div(g.max_box, kQTile);
+  g.groups = g.B * g.boxes * g.heads;
+  g.N = g.T * g.H * g.W;
+}
+
+int64_t win_forward_blocks(const WinGeometry& g) {
+  return (int64_t)ceil_div(g.groups, kXcd) * kXcd * g.qtiles;
+}
+
+hipError_t launch_win_forward(const WinGeometry& g, const void* q, const void* k, const void* v,
+                              void* out, void* out_res, float* lse, hipStream_t s) {
+  const dim3 grid((unsigned)win_forward_blocks(g)), block(kThreads);
+  const uint16_t *qq = static_cast<const uint16_t*>(q), *kk = static_cast<const uint16_t*>(k),
+                 *vv = static_cast<const uint16_t*>(v);
+  uint16_t *oo = static_cast<uint16_t*>(out), *rr = static_cast<uint16_t*>(out_res);
+  void* a[] = {(void*)&g, (void*)&qq, (void*)&kk, (void*)&vv, (void*)&oo, (void*)&rr, (void*)&lse};
+  const void* fn = g.D == 64 ? reinterpret_cast<const void*>(&win_fwd_kernel<64>)
+                             : reinterpret_cast<const void*>(&win_fwd_kernel<128>);
+  return hipLaunchKernel(fn, grid, block, a, 0, s);
+}
+
+hipError_t launch_win_backward(const WinGeometry& g, const void* q, const void* k, const void* v,
+                               const void* out, const void* out_res, const float* lse,
+                               const void* dout, float* dq, float* dk, float* dv,
+                               void* workspace, hipStream_t s, hipEvent_t const* events) {
+  const uint16_t *qq = static_cast<const uint16_t*>(q), *kk = static_cast<const uint16_t*>(k),
+                 *vv = static_cast<const uint16_t*>(v), *oo = static_cast<const uint16_t*>(out),
+                 *rr = static_cast<const uint16_t*>(out_res),
+                 *gg = static_cast<const uint16_t*>(dout);
+  float* delta = static_cast<float*>(workspace);
+  return g.D == 64
+             ? win_backward_d<64>(g, qq, kk, vv, oo, rr, lse, gg, dq, dk, dv, delta, s, events)
+             : win_backward_d<128>(g, qq, kk, vv, oo, rr, lse, gg, dq, dk, dv, delta, s, events);
+}
+
+}  // namespace dsa3d

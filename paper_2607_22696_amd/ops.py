@@ -10,8 +10,9 @@ import torch
 from ._binding import (dsa3d_backward, dsa3d_backward_timed, dsa3d_backward_workspace_size,
                        dsa3d_dwconv3d_backward, dsa3d_dwconv3d_backward_workspace_size,
                        dsa3d_dwconv3d_forward, dsa3d_forward, dsa3d_pw_backward,
-                       dsa3d_pw_backward_workspace_size, dsa3d_pw_forward, make_conv_desc,
-                       make_desc)
+                       dsa3d_pw_backward_workspace_size, dsa3d_pw_forward, dsa3d_win_backward,
+                       dsa3d_win_backward_workspace_size, dsa3d_win_forward, make_conv_desc,
+                       make_desc, make_win_desc)
 
 
 def _desc(q, kernel, scale):
@@ -144,3 +145,46 @@ def pw_backward(logits, v, offsets, lse, dout, kernel=(3, 3, 3), grads=None, wor
                       events=phase_events)
     return dlog, dv, doff
 
+
+def _win_desc(q, window, shift, scale):
+    if q.dim() != 6 or q.dtype != torch.bfloat16:
+        raise ValueError("q must be a bfloat16 [B, T, H, W, heads, head_dim] tensor")
+    B, T, H, W, heads, D = q.shape
+    return make_win_desc(B, T, H, W, heads, D, window, shift, "bf16", scale)
+
+
+def win_forward(q, k, v, window=(3, 16, 16), shift=(0, 0, 0), scale=0.0, need_lse=True,
+                need_residual=True, out=None, lse=None, out_res=None):
+    """Fixed / shifted window attention (bf16).  Returns (out, lse, out_res); out_res, the bf16
+    rounding residual of out that the backward uses for an exact Delta, is None when
+    need_residual is False (and lse when need_lse is False)."""
+    desc = _win_desc(q, window, shift, scale)
+    for name, t in (("k", k), ("v", v)):
+        _check(name, t, q.shape, q.dtype)
+    if out is None:
+        out = torch.empty_like(q)
+    if need_lse and lse is None:
+        lse = torch.empty(q.shape[:5], dtype=torch.float32, device=q.device)
+    if need_residual and out_res is None:
+        out_res = torch.empty_like(q)
+    dsa3d_win_forward(desc, q, k, v, out, out_res if need_residual else None,
+                      lse if need_lse else None)
+    return out, (lse if need_lse else None), (out_res if need_residual else None)
+
+
+def win_backward(q, k, v, out, out_res, lse, dout, window=(3, 16, 16), shift=(0, 0, 0),
+                 scale=0.0, grads=None, workspace=None, phase_events=None):
+    """Returns (dq, dk, dv), float32.  out_res may be None (Delta from the rounded out alone).
+    `phase_events`: optional DSA3D_WIN_BACKWARD_PHASES + 1 created torch.cuda.Event objects
+    marking the two passes."""
+    desc = _win_desc(q, window, shift, scale)
+    if grads is None:
+        f32 = dict(dtype=torch.float32, device=q.device)
+        grads = tuple(torch.empty(q.shape, **f32) for _ in range(3))
+    dq, dk, dv = grads
+    need = dsa3d_win_backward_workspace_size(desc)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    dsa3d_win_backward(desc, q, k, v, out, out_res, lse, dout, dq, dk, dv, workspace, need,
+                       events=phase_events)
+    return dq, dk, dv

@@ -293,3 +293,64 @@ CONV_WORKLOADS = {
     "dwconv_64x34x60": ConvWorkload("dwconv_64x34x60", 1, 64, 34, 60, 1024, 3, 3, 3, "bf16",
                                     seed=21),
 }
+
+
+# ----------------------------------------------------------------------------- window attention
+
+TID_WIN_Q, TID_WIN_K, TID_WIN_V, TID_WIN_DOUT = 30, 31, 32, 33
+
+
+@dataclasses.dataclass(frozen=True)
+class WinWorkload:
+    """A synthetic fixed / shifted window attention problem: bf16 q, k, v and dout ~ N(0, 1)
+    on a T x H x W grid, windows of wt x wh x ww tokens, cyclic shift (st, sh, sw)."""
+    name: str
+    B: int
+    T: int
+    H: int
+    W: int
+    heads: int
+    head_dim: int
+    window: tuple
+    shift: tuple
+    seed: int
+    dtype: str = "bf16"
+
+    @property
+    def N(self):
+        return self.T * self.H * self.W
+
+    @property
+    def queries(self):
+        return self.B * self.N * self.heads
+
+    def shape12(self):
+        return (self.B, self.T, self.H, self.W, self.heads, self.head_dim) + tuple(self.window) + \
+            tuple(self.shift)
+
+    def qkv_shape(self):
+        return (self.B, self.T, self.H, self.W, self.heads, self.head_dim)
+
+    def with_grid(self, **kw) -> "WinWorkload":
+        return dataclasses.replace(self, **kw)
+
+
+def gen_win_inputs(w: WinWorkload, progress=None):
+    """Host copies (bf16 bit patterns) of q, k, v and dout."""
+    out = []
+    for name, tid in (("q", TID_WIN_Q), ("k", TID_WIN_K), ("v", TID_WIN_V), ("dout", TID_WIN_DOUT)):
+        if progress is not None:
+            progress(f"generating {name} {w.qkv_shape()} of {w.name}")
+        out.append(fill(np.empty(w.qkv_shape(), dtype=np.uint16), w.seed, tid, 0, N01))
+    return tuple(out)
+
+
+WIN_WORKLOADS = {
+    # Swin-DiT's attention (Section 6.2): shifted 3 x 16 x 16 windows on 256 frames of 1080p,
+    # 2,088,960 tokens, 24 heads x 128.
+    "swin_1080p_256f": WinWorkload("swin_1080p_256f", 1, 256, 68, 120, 24, 128, (3, 16, 16),
+                                   (1, 8, 8), seed=30),
+    # The same windows on the forward + backward grid: 130,560 tokens, 16 heads x 64.
+    "swin_64x34x60": WinWorkload("swin_64x34x60", 1, 64, 34, 60, 16, 64, (3, 16, 16), (1, 8, 8),
+                                 seed=31),
+}

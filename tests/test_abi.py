@@ -348,3 +348,94 @@ def test_pw_workspace_is_the_backward_binning():
         d = good_desc(**kw)
         assert dsa.dsa3d_pw_backward_workspace_size(d) == dsa.dsa3d_backward_workspace_size(d) > 0
     assert dsa.dsa3d_pw_backward_workspace_size(good_desc(scale=2.0)) == 0
+
+
+# ----------------------------------------------------------------------------- window attention
+
+def good_win(**over):
+    kw = dict(B=1, T=6, H=20, W=24, heads=2, head_dim=64, window=(3, 16, 16), shift=(1, 8, 8))
+    kw.update(over)
+    return dsa.make_win_desc(kw["B"], kw["T"], kw["H"], kw["W"], kw["heads"], kw["head_dim"],
+                             kw["window"], kw["shift"], kw.get("dtype", "bf16"), kw.get("scale", 0.0))
+
+
+def win_fwd(desc, **over):
+    q, k, v, out, res, lse = ptrs(6)
+    args = dict(q=q, k=k, v=v, out=out, out_res=res, lse=lse)
+    args.update(over)
+    return dsa.dsa3d_win_forward(desc, args["q"], args["k"], args["v"], args["out"],
+                                 args["out_res"], args["lse"], stream=0, check=False)
+
+
+def win_bwd(desc, **over):
+    names = ["q", "k", "v", "out", "out_res", "lse", "dout", "dq", "dk", "dv", "workspace"]
+    args = dict(zip(names, ptrs(len(names))))
+    args["workspace_bytes"] = 1 << 33
+    args.update(over)
+    return dsa.dsa3d_win_backward(desc, *[args[n] for n in names[:-1]], workspace=args["workspace"],
+                                  workspace_bytes=args["workspace_bytes"], stream=0, check=False)
+
+
+def test_win_desc_layout_matches_header():
+    # 12 int32 dims + float scale + enum dtype
+    assert ctypes.sizeof(B.dsa3d_win_desc) == 14 * 4
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(T=0), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(heads=0), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(window=(0, 16, 16)), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(shift=(3, 8, 8)), B.DSA3D_ERR_INVALID_SHAPE),      # shift must be below the window
+    (dict(shift=(-1, 0, 0)), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(scale=-1.0), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(scale=float("nan")), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(window=(2, 256, 256), shift=(0, 0, 0)), B.DSA3D_ERR_INVALID_SHAPE),  # > 65536 tokens
+    (dict(B=1 << 12, T=1 << 10, H=1 << 5, W=1 << 4, heads=1), B.DSA3D_ERR_INVALID_SHAPE),  # 2^31 rows
+    (dict(W=1 << 24, H=1, T=1), B.DSA3D_ERR_INVALID_SHAPE),
+    (dict(dtype="f32"), B.DSA3D_ERR_UNSUPPORTED),
+    (dict(head_dim=32), B.DSA3D_ERR_UNSUPPORTED),
+    (dict(head_dim=96), B.DSA3D_ERR_UNSUPPORTED),
+])
+def test_win_descriptor_errors(over, status):
+    d = good_win(**over)
+    assert win_fwd(d) == status
+    assert win_bwd(d) == status
+    assert dsa.dsa3d_win_backward_workspace_size(d) == 0
+
+
+def test_win_pointer_checks():
+    d = good_win()
+    assert win_fwd(None) == B.DSA3D_ERR_NULL_POINTER
+    for name in ["q", "k", "v", "out"]:
+        assert win_fwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+    for name in ["q", "k", "v", "out", "lse", "dout", "dq", "dk", "dv"]:
+        assert win_bwd(d, **{name: None}) == B.DSA3D_ERR_NULL_POINTER, name
+    far = ptrs(16)[15]
+    for name in ["q", "k", "v", "out", "out_res"]:
+        assert win_fwd(d, **{name: far + 8}) == B.DSA3D_ERR_MISALIGNED, name
+    assert win_fwd(d, lse=far + 2) == B.DSA3D_ERR_MISALIGNED
+    for name in ["out_res", "dout", "dq", "dk", "dv"]:
+        assert win_bwd(d, **{name: far + 8}) == B.DSA3D_ERR_MISALIGNED, name
+    assert win_bwd(d, workspace=far + 128) == B.DSA3D_ERR_MISALIGNED
+    f = ptrs(6)
+    assert win_fwd(d, out=f[0] + 256) == B.DSA3D_ERR_ALIAS               # out inside q
+    assert win_fwd(d, lse=f[3] + 64) == B.DSA3D_ERR_ALIAS                # lse inside out
+    assert win_fwd(d, out_res=f[3]) == B.DSA3D_ERR_ALIAS                 # out_res == out
+    assert win_fwd(d, out_res=f[1] + 16) == B.DSA3D_ERR_ALIAS            # out_res inside k
+    names = ptrs(11)
+    assert win_bwd(d, dk=names[7]) == B.DSA3D_ERR_ALIAS                  # dk == dq
+    assert win_bwd(d, dv=names[6]) == B.DSA3D_ERR_ALIAS                  # dv == dout
+    assert win_bwd(d, dq=names[4]) == B.DSA3D_ERR_ALIAS                  # dq == out_res
+    assert win_bwd(d, workspace=names[9]) == B.DSA3D_ERR_ALIAS           # workspace == dv
+
+
+def test_win_workspace_size_and_errors():
+    for over in (dict(), dict(B=2, T=5, H=7, W=9, heads=3, head_dim=128, window=(2, 3, 5),
+                                 shift=(1, 1, 2))):
+        d = good_win(**over)
+        rows = d.batch * d.frames * d.height * d.width * d.heads
+        assert dsa.dsa3d_win_backward_workspace_size(d) == -(-rows * 4 // 256) * 256
+    d = good_win()
+    need = dsa.dsa3d_win_backward_workspace_size(d)
+    assert win_bwd(d, workspace=None) == B.DSA3D_ERR_WORKSPACE
+    assert win_bwd(d, workspace_bytes=need - 1) == B.DSA3D_ERR_WORKSPACE

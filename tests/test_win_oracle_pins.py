@@ -144,3 +144,17 @@ def test_bf16_inputs_are_read_exactly():
     np.testing.assert_array_equal(ga[0], gb[0])   # dq: per query
     for x, y in zip(ga[1:], gb[1:]):              # dk, dv: OpenMP atomic summation order
         np.testing.assert_allclose(x, y, rtol=0, atol=1e-12)
+
+
+def test_backward_frame_range_is_exact_on_whole_regions():
+    """With shift 1 and windows of 3 frames the temporal regions are frames [0,1), [1,4), [4,6):
+    the backward over the queries of [1, 4) gives the full dq there, and the full dk, dv of keys
+    in those frames (their queries all lie in the same frames)."""
+    B, T, H, W, M, D = 1, 6, 5, 6, 2, 4
+    shape = (B, T, H, W, M, D, 3, 4, 4, 1, 2, 2)
+    q, k, v, dout = (rand((B, T, H, W, M, D), s) for s in (15, 16, 17, 18))
+    full = oracle.win_backward(shape, "f32", q, k, v, dout)
+    part = oracle.win_backward(shape, "f32", q, k, v, dout, frames=(1, 4))
+    for a, b in zip(part, full):
+        assert a.shape == (B, 3, H, W, M, D)
+        np.testing.assert_allclose(a, b[:, 1:4], rtol=0, atol=1e-12)
