@@ -32,6 +32,9 @@ DEFAULT_CONV_WORKLOAD = "dwconv_1080p_256f"
 DEFAULT_PW_WORKLOAD = "pw_64x34x60"
 PW_METRIC = "3D-DSA predicted-weights fwd+bwd queries/s and achieved HBM GB/s (% of peak) at 1 GPU"
 CONV_METRIC = "DWConv3D fwd+bwd tokens/s and achieved HBM GB/s (% of peak) at 1 GPU"
+WIN_METRIC = "Swin-DiT shifted-window attention fwd+bwd queries/s and MFMA TFLOP/s (% of peak) at 1 GPU"
+DEFAULT_WIN_WORKLOAD = "swin_1080p_256f"
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2607_22696_amd", "csrc")
 
@@ -40,6 +43,7 @@ CSRC = os.path.join(ROOT, "paper_2607_22696_amd", "csrc")
 FAMILY_SOURCES = {
     "dsa": ["dsa3d_device.h", "dsa3d_forward.hip", "dsa3d_backward.hip"],
     "dwconv": ["dsa3d_device.h", "dwconv3d.hip"],
+    "win": ["winattn.hip"],
 }
 
 
@@ -54,7 +58,9 @@ def kernel_source_hash(family: str = "dsa") -> str:
 
 
 def workload_family(workload: str) -> str:
-    return "dwconv" if workload.startswith("dwconv") else "dsa"
+    if workload.startswith("dwconv"):
+        return "dwconv"
+    return "win" if workload.startswith("swin") else "dsa"
 
 
 def kernel_base(name: str) -> str:
@@ -421,15 +427,157 @@ def bench_pw(args, torch, dsa, testgen, to_device):
     print(json.dumps(res), flush=True)
 
 
+def win_boxes(w):
+    """Sizes of the boxes the shifted windows cut the grid into: along each axis the cuts are
+    shift + n * window (plus the grid ends); a query attends to every token of its box."""
+    import numpy as np
+
+    def axis(size, win, shift):
+        off = shift - win if shift > 0 else 0
+        n = -(-(size - off) // win)
+        lo = np.maximum(off + win * np.arange(n), 0)
+        hi = np.minimum(off + win * (np.arange(n) + 1), size)
+        return hi - lo
+
+    lt = axis(w.T, w.window[0], w.shift[0])
+    lh = axis(w.H, w.window[1], w.shift[1])
+    lw = axis(w.W, w.window[2], w.shift[2])
+    return (lt[:, None, None] * lh[None, :, None] * lw[None, None, :]).ravel()
+
+
+def win_algorithmic(w):
+    """Algorithmic FLOPs (and HBM bytes) per launch of the window-attention kernels.  A box of n
+    tokens and one head costs 2 n^2 D FLOPs per n x n x D product (a multiply-add is 2 FLOPs):
+      win_fwd_kernel   S = Q K^T and O = P V: 4 n^2 D; reads q, k, v, writes out, out_res (bf16)
+                       and lse
+      win_dq_kernel    S, dP = dout V^T and dq = dS K: 6 n^2 D; reads q, k, v, out, out_res,
+                       dout, lse, writes dq (fp32) and Delta
+      win_dkdv_kernel  S, dP, dV = P^T dout and dK = dS^T Q: 8 n^2 D; reads q, k, v, dout, lse,
+                       Delta, writes dk, dv (fp32)
+      backward         the two passes (S and dP are formed in both)
+    The kernels take P and dS into the products as bf16 hi + lo pairs, which executes 2 n^2 D
+    more per such product (6, 8 and 12 n^2 D instead of 4, 6 and 8); those are not counted."""
+    n2 = float((win_boxes(w).astype("float64") ** 2).sum())
+    per = w.B * w.heads * n2 * w.head_dim
+    rows = w.queries
+    D = w.head_dim
+    work = {
+        "win_fwd_kernel": (rows * (5 * 2 * D + 4), 4 * per),
+        "win_dq_kernel": (rows * (6 * 2 * D + 4 * D + 8), 6 * per),
+        "win_dkdv_kernel": (rows * (4 * 2 * D + 8 * D + 8), 8 * per),
+    }
+    work["backward"] = (work["win_dq_kernel"][0] + work["win_dkdv_kernel"][0], 14 * per)
+    return {k: {"bytes": b, "flops": f} for k, (b, f) in work.items()}
+
+
+def mfma_roofline(work, ms):
+    ach = work["flops"] / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4)}
+
+
+def bench_win(args, torch, dsa, testgen, to_device):
+    """One step = forward (with the output residual) and backward of the shifted-window
+    attention."""
+    w = testgen.WIN_WORKLOADS[args.workload]
+    t_gen = time.perf_counter()
+    host = testgen.gen_win_inputs(w, progress=lambda m: print(m, file=sys.stderr, flush=True))
+    print("copying inputs to the GPU", file=sys.stderr, flush=True)
+    qd, kd, vd, gd = (to_device(a, True) for a in host)
+    t_gen = time.perf_counter() - t_gen
+    print(f"inputs resident after {t_gen:.1f} s; timing", file=sys.stderr, flush=True)
+    kw = dict(window=w.window, shift=w.shift)
+    out, lse, res = dsa.win_forward(qd, kd, vd, **kw)
+    f32 = dict(dtype=torch.float32, device=qd.device)
+    grads = tuple(torch.empty(qd.shape, **f32) for _ in range(3))
+    need = dsa.dsa3d_win_backward_workspace_size(dsa.make_win_desc(
+        w.B, w.T, w.H, w.W, w.heads, w.head_dim, w.window, w.shift))
+    workspace = torch.empty(need, dtype=torch.uint8, device=qd.device)
+
+    def new_events(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:
+            e.record()
+        return evs
+
+    K = args.steps
+    ev = [new_events(2) for _ in range(K)]
+    ph = [new_events(dsa.DSA3D_WIN_BACKWARD_PHASES + 1) for _ in range(K)]
+
+    def step(s=None):
+        if s is not None:
+            ev[s][0].record()
+        dsa.win_forward(qd, kd, vd, out=out, lse=lse, out_res=res, **kw)
+        if s is not None:
+            ev[s][1].record()
+        dsa.win_backward(qd, kd, vd, out, res, lse, gd, grads=grads, workspace=workspace,
+                         phase_events=None if s is None else ph[s], **kw)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for s in range(K):
+        step(s)
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / K
+    kernel_ms = {"win_fwd_kernel": sum(e[0].elapsed_time(e[1]) for e in ev) / K}
+    for i, n in enumerate(["win_dq_kernel", "win_dkdv_kernel"]):
+        kernel_ms[n] = sum(p[i].elapsed_time(p[i + 1]) for p in ph) / K
+    alg = win_algorithmic(w)
+    kname = max(kernel_ms, key=lambda n: kernel_ms[n])
+    roof = mfma_roofline(alg[kname], kernel_ms[kname])
+    roof["traffic"] = measured_traffic(w.name, kname)
+    roof["kernel"] = kname
+    roof["avg_launch_ms"] = round(kernel_ms[kname], 4)
+    step_flops = alg["win_fwd_kernel"]["flops"] + alg["backward"]["flops"]
+    res_json = {
+        "metric": WIN_METRIC, "value": round(w.B * w.N / (ms_step * 1e-3), 1), "unit": "queries/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Philox inputs shaped like the paper's video-latent grids)",
+        "config": {"workload": w.name, "grid_TxHxW": [w.T, w.H, w.W], "batch": w.B,
+                   "heads": w.heads, "head_dim": w.head_dim, "window": list(w.window),
+                   "shift": list(w.shift), "backward": True, "parallelism": "single GPU"},
+        "kernel_ms": {n: round(t, 4) for n, t in kernel_ms.items()},
+        "kernel_roofline": {n: mfma_roofline(alg[n], t) for n, t in kernel_ms.items()},
+        "step_tflops_algorithmic": round(step_flops / (ms_step * 1e-3) / 1e12, 2),
+        "step_mfma_frac_algorithmic": round(step_flops / (ms_step * 1e-3) / 1e12
+                                            / MFMA_BF16_PEAK_TFLOPS, 4),
+        "roofline": roof, "input_gen_s": round(t_gen, 1),
+    }
+    if args.cpu_budget > 0:
+        import oracle
+        q, k, v, dout = host
+        frames = []
+        t0 = time.perf_counter()
+        f = min(1, w.T - 1)
+        while f < w.T and time.perf_counter() - t0 < args.cpu_budget:
+            oracle.win_forward(w.shape12(), "bf16", q, k, v, frames=(f, f + 1))
+            oracle.win_backward(w.shape12(), "bf16", q, k, v, dout, frames=(f, f + 1))
+            frames.append(f)
+            f += 1
+        dt = time.perf_counter() - t0
+        res_json["cpu_baseline"] = {
+            "value": round(len(frames) * w.H * w.W * w.B / dt, 2), "unit": "queries/s",
+            "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"frames {frames[0]}..{frames[-1]} of {w.name} (all heads): forward + "
+                      f"backward of their queries, fp64, {dt:.1f} s"}
+    print(json.dumps(res_json), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--op", choices=["dsa", "dwconv", "pw"], default="dsa",
+    ap.add_argument("--op", choices=["dsa", "dwconv", "pw", "win"], default="dsa",
                     help="dsa: the 3D-DSA operator (default); dwconv: the depthwise 3D "
                          "convolution term of Eq. (1) (workloads dwconv_*); pw: the "
-                         "predicted-weights variant (workloads pw_*)")
+                         "predicted-weights variant (workloads pw_*); win: the Swin-DiT "
+                         "shifted-window attention (workloads swin_*)")
     ap.add_argument("--workload", default=None,
                     help=f"default {DEFAULT_WORKLOAD} (dsa) or {DEFAULT_CONV_WORKLOAD} (dwconv)")
     ap.add_argument("--forward-only", action="store_true",
@@ -445,8 +593,8 @@ def main():
     args = ap.parse_args()
 
     if args.workload is None:
-        args.workload = {"dwconv": DEFAULT_CONV_WORKLOAD, "pw": DEFAULT_PW_WORKLOAD}.get(
-            args.op, DEFAULT_WORKLOAD)
+        args.workload = {"dwconv": DEFAULT_CONV_WORKLOAD, "pw": DEFAULT_PW_WORKLOAD,
+                         "win": DEFAULT_WIN_WORKLOAD}.get(args.op, DEFAULT_WORKLOAD)
     if args.pmc_summary:
         pmc_summary(args.workload, *args.pmc_summary, copy_mib=args.copy_probe or 1024)
         return
@@ -485,6 +633,9 @@ def main():
         return
     if args.op == "pw":
         bench_pw(args, torch, dsa, testgen, to_device)
+        return
+    if args.op == "win":
+        bench_win(args, torch, dsa, testgen, to_device)
         return
     w = testgen.WORKLOADS[args.workload]
     do_bwd = w.backward and not args.forward_only
