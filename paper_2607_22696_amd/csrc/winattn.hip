@@ -35,6 +35,7 @@ constexpr int kTile = 64;    // rows per LDS tile (keys of the forward and dq pa
                              // of the dk/dv pass)
 constexpr int kXcd = 8;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kSlack = 8.0f;  // base-2 headroom of the forward's running maximum
 
 struct Box {
   int t0, i0, j0, lh, lw, n;
@@ -104,6 +105,15 @@ __device__ inline uint32_t pick_pair(uint32_t k1, uint32_t k0, bool high) {
   return __builtin_amdgcn_perm(k1, k0, high ? 0x07060302u : 0x05040100u);
 }
 
+// Tensor rows of tile rows base .. base + kTile - 1 of the group's box (-1 past the box end),
+// computed by the first wave for the whole workgroup.
+__device__ inline void fill_rows(int* tab, const WinGeometry& g, const Group& gr, int base) {
+  if (threadIdx.x < kTile) {
+    const int u = base + threadIdx.x;
+    tab[threadIdx.x] = u < gr.bx.n ? (int)row_of(g, gr.b, box_token(g, gr.bx, u), gr.m) : -1;
+  }
+}
+
 // Staging of a tile of kTile box rows (box-local indices base .. base + kTile - 1; rows past the
 // box end read as zero) of a [rows][D] bf16 tensor into LDS, gathered through the box's token
 // order.  Row-major tiles keep rows of D channels (pitch D + 8: 16-byte reads of 8 lanes on 8
@@ -120,17 +130,22 @@ struct Tile {
   static constexpr int kColElems = D * TP;
   static_assert(NL == 2 || NL == 4, "head_dim 64 or 128");
 
-  // Row-major: thread t moves chunk t % KCH of rows t / KCH + r * (kThreads / KCH).
-  static __device__ inline void load_rows(uint4 (&r)[NL], const uint16_t* src, const WinGeometry& g,
-                                          const Group& gr, int base) {
+  // Row-major: thread t moves chunk t % KCH of tile rows t / KCH + i * (kThreads / KCH).
+  // tab[r] is the tensor row of tile row r, or -1 past the box end (read as zero).
+  // full: every row of the tile lies in the box (no checks, the common case).
+  static __device__ inline void load_rows(uint4 (&r)[NL], const uint16_t* src, const int* tab,
+                                          bool full) {
     const int t = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
-      const int u = base + t / KCH + i * (kThreads / KCH);
-      r[i] = make_uint4(0, 0, 0, 0);
-      if (u < gr.bx.n)
-        r[i] = *reinterpret_cast<const uint4*>(
-            src + row_of(g, gr.b, box_token(g, gr.bx, u), gr.m) * D + (t % KCH) * 8);
+      const int row = tab[t / KCH + i * (kThreads / KCH)];
+      const uint4* at = reinterpret_cast<const uint4*>(src + (int64_t)row * D + (t % KCH) * 8);
+      if (full) {
+        r[i] = *at;
+      } else {
+        r[i] = make_uint4(0, 0, 0, 0);
+        if (row >= 0) r[i] = *at;
+      }
     }
   }
   static __device__ inline void store_rows(uint16_t* lds, const uint4 (&r)[NL]) {
@@ -140,18 +155,21 @@ struct Tile {
       *reinterpret_cast<uint4*>(lds + (t / KCH + i * (kThreads / KCH)) * RP + (t % KCH) * 8) = r[i];
   }
 
-  // Transposed: thread t moves chunk t / VG of rows (t % VG) * NL + e, e < NL, and writes, for
-  // each of the chunk's 8 channels, its NL rows as one 4- or 8-byte word.
-  static __device__ inline void load_cols(uint4 (&r)[NL], const uint16_t* src, const WinGeometry& g,
-                                          const Group& gr, int base) {
+  // Transposed: thread t moves chunk t / VG of tile rows (t % VG) * NL + e, e < NL, and
+  // writes, for each of the chunk's 8 channels, its NL rows as one 4- or 8-byte word.
+  static __device__ inline void load_cols(uint4 (&r)[NL], const uint16_t* src, const int* tab,
+                                          bool full) {
     const int t = threadIdx.x;
 #pragma unroll
     for (int e = 0; e < NL; ++e) {
-      const int u = base + (t % VG) * NL + e;
-      r[e] = make_uint4(0, 0, 0, 0);
-      if (u < gr.bx.n)
-        r[e] = *reinterpret_cast<const uint4*>(
-            src + row_of(g, gr.b, box_token(g, gr.bx, u), gr.m) * D + (t / VG) * 8);
+      const int row = tab[(t % VG) * NL + e];
+      const uint4* at = reinterpret_cast<const uint4*>(src + (int64_t)row * D + (t / VG) * 8);
+      if (full) {
+        r[e] = *at;
+      } else {
+        r[e] = make_uint4(0, 0, 0, 0);
+        if (row >= 0) r[e] = *at;
+      }
     }
   }
   static __device__ inline void store_cols(uint16_t* lds, const uint4 (&r)[NL]) {
@@ -206,15 +224,25 @@ __device__ inline void load_frag(bf16x8_t (&f)[D / 16], const uint16_t* src, int
 }
 
 // Sixteen C-layout values as B-operand fragments (elements 8 p .. 8 p + 7) of a bf16 pair
-// hi + lo: hi = bf16(x), lo = bf16(x - hi).  The pair carries about 16 significant bits, so a
-// product taken as two MFMAs (hi and lo) loses almost nothing to the bf16 operand.
+// hi + lo carrying about 16 significant bits, so a product taken as two MFMAs (hi and lo)
+// loses almost nothing to the bf16 operand.
 __device__ inline void to_frags(const float (&x)[16], bf16x8_t (&hi)[2], bf16x8_t (&lo)[2]) {
+  // hi = x truncated to its upper 16 bits (two of them packed by one byte permute); lo = x - hi
+  // is exact in fp32 and rounded once to bf16, so hi + lo is x to within 2^-17 |x|.
+  uint32_t h[8], l[8];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const __bf16 h = (__bf16)x[i];
-    hi[i / 8][i % 8] = h;
-    lo[i / 8][i % 8] = (__bf16)(x[i] - (float)h);
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t u0 = __float_as_uint(x[2 * i]), u1 = __float_as_uint(x[2 * i + 1]);
+    h[i] = __builtin_amdgcn_perm(u1, u0, 0x07060302u);
+    const float l0 = x[2 * i] - __uint_as_float(u0 & 0xffff0000u);
+    const float l1 = x[2 * i + 1] - __uint_as_float(u1 & 0xffff0000u);
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    l[i] = __builtin_bit_cast(uint32_t, bf16x2_t{(__bf16)l0, (__bf16)l1});
   }
+  hi[0] = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+  hi[1] = __builtin_bit_cast(bf16x8_t, make_uint4(h[4], h[5], h[6], h[7]));
+  lo[0] = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
+  lo[1] = __builtin_bit_cast(bf16x8_t, make_uint4(l[4], l[5], l[6], l[7]));
 }
 
 // Stores this lane's 16 fp32 C-layout values of channel block db (channels 32 db + 8 blk +
@@ -249,11 +277,13 @@ win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __
   constexpr int DB = D / 32;  // 32-channel blocks of the output
   __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kRowElems];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[Tl::kColElems];
+  __shared__ int tab[2][kTile];  // key rows of the current and the next tile
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int q0 = gr.qt * kQTile, n = gr.bx.n;
   if (q0 >= n) return;  // the box has fewer tiles than the largest one
+  fill_rows(tab[0], g, gr, 0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uq = q0 + wave * 32 + (lane & 31);
@@ -269,15 +299,18 @@ win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __
 
   uint4 kr[Tl::NL], vr[Tl::NL];
   const int ntiles = (n + kTile - 1) / kTile;
-  Tl::load_rows(kr, k, g, gr, 0);
-  Tl::load_cols(vr, v, g, gr, 0);
+  __syncthreads();
+  Tl::load_rows(kr, k, tab[0], kTile <= n);
+  Tl::load_cols(vr, v, tab[0], kTile <= n);
   for (int kt = 0; kt < ntiles; ++kt) {
     Tl::store_rows(Ks, kr);
     Tl::store_cols(Vt, vr);
+    if (kt + 1 < ntiles) fill_rows(tab[(kt + 1) & 1], g, gr, (kt + 1) * kTile);
     __syncthreads();
     if (kt + 1 < ntiles) {
-      Tl::load_rows(kr, k, g, gr, (kt + 1) * kTile);
-      Tl::load_cols(vr, v, g, gr, (kt + 1) * kTile);
+      const bool full = (kt + 2) * kTile <= n;
+      Tl::load_rows(kr, k, tab[(kt + 1) & 1], full);
+      Tl::load_cols(vr, v, tab[(kt + 1) & 1], full);
     }
 
     // S^T = K Q^T for the two 32-key blocks of the tile
@@ -303,13 +336,20 @@ win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(sm.m, mx * g.scale_log2);  // scale > 0
-    const float corr = __builtin_amdgcn_exp2f(sm.m - mnew);
-    sm.m = mnew;
-    sm.l *= corr;
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * g.scale_log2;  // scale > 0
+    // The running maximum is raised only when a logit exceeds it by more than kSlack (base 2),
+    // so P stays below 2^kSlack and the rescale of O is skipped by whole waves most of the
+    // time; the result does not depend on which maximum was used.
+    const bool raise = mx > sm.m + kSlack;
+    if (__any(raise)) {
+      const float mnew = raise ? mx : sm.m;
+      const float corr = __builtin_amdgcn_exp2f(sm.m - mnew);
+      sm.m = mnew;
+      sm.l *= corr;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) o[db] *= corr;
+      for (int db = 0; db < DB; ++db) o[db] *= corr;
+    }
+    const float mnew = sm.m;
 
     bf16x8_t ph[2][2], pl[2][2];  // P^T as B-operand fragments (hi + lo)
 #pragma unroll
@@ -377,11 +417,13 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
   __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kRowElems];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[Tl::kRowElems];
   __shared__ __attribute__((aligned(16))) uint16_t Kt[Tl::kColElems];
+  __shared__ int tab[2][kTile];  // key rows of the current and the next tile
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int q0 = gr.qt * kQTile, n = gr.bx.n;
   if (q0 >= n) return;
+  fill_rows(tab[0], g, gr, 0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uq = q0 + wave * 32 + (lane & 31);
@@ -412,18 +454,22 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
 
   uint4 kr[Tl::NL], vr[Tl::NL], kc[Tl::NL];
   const int ntiles = (n + kTile - 1) / kTile;
-  Tl::load_rows(kr, k, g, gr, 0);
-  Tl::load_rows(vr, v, g, gr, 0);
-  Tl::load_cols(kc, k, g, gr, 0);
+  __syncthreads();
+  Tl::load_rows(kr, k, tab[0], kTile <= n);
+  Tl::load_rows(vr, v, tab[0], kTile <= n);
+  Tl::load_cols(kc, k, tab[0], kTile <= n);
   for (int kt = 0; kt < ntiles; ++kt) {
     Tl::store_rows(Ks, kr);
     Tl::store_rows(Vs, vr);
     Tl::store_cols(Kt, kc);
+    if (kt + 1 < ntiles) fill_rows(tab[(kt + 1) & 1], g, gr, (kt + 1) * kTile);
     __syncthreads();
     if (kt + 1 < ntiles) {
-      Tl::load_rows(kr, k, g, gr, (kt + 1) * kTile);
-      Tl::load_rows(vr, v, g, gr, (kt + 1) * kTile);
-      Tl::load_cols(kc, k, g, gr, (kt + 1) * kTile);
+      const int* t1 = tab[(kt + 1) & 1];
+      const bool full = (kt + 2) * kTile <= n;
+      Tl::load_rows(kr, k, t1, full);
+      Tl::load_rows(vr, v, t1, full);
+      Tl::load_cols(kc, k, t1, full);
     }
     const int kbase = kt * kTile;
 #pragma unroll
@@ -477,11 +523,13 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
   __shared__ __attribute__((aligned(16))) uint16_t Gt[Tl::kColElems];
   __shared__ __attribute__((aligned(16))) float Ls[kTile];  // lse log2(e); +inf past the box end
   __shared__ __attribute__((aligned(16))) float Dl[kTile];  // Delta
+  __shared__ int tab[2][kTile];  // query rows of the current and the next tile
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int k0 = gr.qt * kQTile, n = gr.bx.n;
   if (k0 >= n) return;
+  fill_rows(tab[0], g, gr, 0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uk = k0 + wave * 32 + (lane & 31);
@@ -495,32 +543,39 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
 #pragma unroll
   for (int db = 0; db < DB; ++db) dka[db] = dva[db] = f32x16_t{};
 
-  const int ntiles = (n + kTile - 1) / kTile;
-  for (int qt = 0; qt < ntiles; ++qt) {
-    const int qbase = qt * kTile;
-    {
-      uint4 r[Tl::NL];
-      Tl::load_rows(r, q, g, gr, qbase);
-      Tl::store_rows(Qs, r);
-      Tl::load_cols(r, q, g, gr, qbase);
-      Tl::store_cols(Qt, r);
-      Tl::load_rows(r, dout, g, gr, qbase);
-      Tl::store_rows(Gs, r);
-      Tl::load_cols(r, dout, g, gr, qbase);
-      Tl::store_cols(Gt, r);
-      if (threadIdx.x < kTile) {
-        const int u = qbase + threadIdx.x;
-        float ls = INFINITY, de = 0.0f;
-        if (u < n) {
-          const int64_t row = row_of(g, gr.b, box_token(g, gr.bx, u), gr.m);
-          ls = lse[row] * 1.4426950408889634f;
-          de = delta[row];
-        }
-        Ls[threadIdx.x] = ls;
-        Dl[threadIdx.x] = de;
+  // the next query tile is fetched into registers while the current one is used
+  uint4 rq[Tl::NL], cq[Tl::NL], rg[Tl::NL], cg[Tl::NL];
+  float ls = INFINITY, de = 0.0f;
+  auto fetch = [&](const int* t1, bool full) {
+    Tl::load_rows(rq, q, t1, full);
+    Tl::load_cols(cq, q, t1, full);
+    Tl::load_rows(rg, dout, t1, full);
+    Tl::load_cols(cg, dout, t1, full);
+    if (threadIdx.x < kTile) {
+      const int row = t1[threadIdx.x];
+      ls = INFINITY;
+      de = 0.0f;
+      if (row >= 0) {
+        ls = lse[row] * 1.4426950408889634f;
+        de = delta[row];
       }
     }
+  };
+  const int ntiles = (n + kTile - 1) / kTile;
+  __syncthreads();
+  fetch(tab[0], kTile <= n);
+  for (int qt = 0; qt < ntiles; ++qt) {
+    Tl::store_rows(Qs, rq);
+    Tl::store_cols(Qt, cq);
+    Tl::store_rows(Gs, rg);
+    Tl::store_cols(Gt, cg);
+    if (threadIdx.x < kTile) {
+      Ls[threadIdx.x] = ls;
+      Dl[threadIdx.x] = de;
+    }
+    if (qt + 1 < ntiles) fill_rows(tab[(qt + 1) & 1], g, gr, (qt + 1) * kTile);
     __syncthreads();
+    if (qt + 1 < ntiles) fetch(tab[(qt + 1) & 1], (qt + 2) * kTile <= n);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       f32x16_t sa = f32x16_t{}, pa = f32x16_t{};
