@@ -31,8 +31,8 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
 constexpr int kQTile = 128;  // queries per workgroup: 4 waves x 32
-constexpr int kTile = 64;    // rows per LDS tile (keys of the forward and dq passes, queries
-                             // of the dk/dv pass)
+constexpr int kTile = 64;    // rows per LDS tile of the dq (keys) and dk/dv (queries) passes
+constexpr int kFwdTile = 64;   // keys per LDS tile of the forward
 constexpr int kXcd = 8;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kSlack = 8.0f;  // base-2 headroom of the forward's running maximum
@@ -94,119 +94,105 @@ __device__ inline int64_t row_of(const WinGeometry& g, int b, int tok, int m) {
   return ((int64_t)b * g.N + tok) * g.heads + m;
 }
 
+// x combined with the value of lane l ^ 32 by v_permlane32_swap, which moves data between the
+// two halves of the wave without going through LDS (so it does not wait for outstanding LDS
+// reads).  Applied to (x, x) it returns, in each lane, the lane's own value and its partner's
+// (in either order), so max and sum come out identical in both lanes of a pair.
+__device__ inline float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ inline f32x16_t mfma(const bf16x8_t& a, const bf16x8_t& b, const f32x16_t& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ inline bf16x8_t as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
 
-// Two bf16 of one column of a row pair: keys k0 (low half of the result) and k1.
-__device__ inline uint32_t pick_pair(uint32_t k1, uint32_t k0, bool high) {
-  return __builtin_amdgcn_perm(k1, k0, high ? 0x07060302u : 0x05040100u);
-}
-
-// Tensor rows of tile rows base .. base + kTile - 1 of the group's box (-1 past the box end),
-// computed by the first wave for the whole workgroup.
+// Tensor rows of tile rows base .. base + ROWS - 1 of the group's box, computed by the first
+// ROWS threads for the whole workgroup.  Tile rows past the box end get the box's last row (a
+// valid address: the loads need no branch; the staging zeroes what they read).
+template <int ROWS>
 __device__ inline void fill_rows(int* tab, const WinGeometry& g, const Group& gr, int base) {
-  if (threadIdx.x < kTile) {
-    const int u = base + threadIdx.x;
-    tab[threadIdx.x] = u < gr.bx.n ? (int)row_of(g, gr.b, box_token(g, gr.bx, u), gr.m) : -1;
+  if (threadIdx.x < ROWS) {
+    const int u = min(base + (int)threadIdx.x, gr.bx.n - 1);
+    tab[threadIdx.x] = (int)row_of(g, gr.b, box_token(g, gr.bx, u), gr.m);
   }
 }
 
-// Staging of a tile of kTile box rows (box-local indices base .. base + kTile - 1; rows past the
-// box end read as zero) of a [rows][D] bf16 tensor into LDS, gathered through the box's token
-// order.  Row-major tiles keep rows of D channels (pitch D + 8: 16-byte reads of 8 lanes on 8
-// consecutive rows hit distinct banks); transposed tiles keep, per channel, the kTile rows
-// (pitch kTile + 4).  Each thread moves NL 16-byte chunks.
-template <int D>
+// A tile of ROWS box rows (box-local indices base .. base + ROWS - 1; rows past the box end
+// read as zero) of a [rows][D] bf16 tensor in LDS, gathered through the box's token order.
+// Rows are D channels long, unpadded; within each run of 8 16-byte chunks of a row the chunks
+// are XOR-permuted by f(row) = 2 (row % 4) + (row / 4) % 2.  Then 16-byte reads of one chunk
+// of 8 consecutive rows (the row-major operand) and the transposing 8-byte reads of 4
+// consecutive rows x 32 bytes (the column operand) both hit every bank once.  Each thread
+// stages NL 16-byte chunks.
+template <int D, int ROWS>
 struct Tile {
-  static constexpr int RP = D + 8;                   // row-major pitch (bf16)
-  static constexpr int TP = kTile + 4;               // transposed pitch (bf16)
-  static constexpr int KCH = D / 8;                  // 16-byte chunks per row
-  static constexpr int NL = kTile * KCH / kThreads;  // chunks per thread
-  static constexpr int VG = kTile / NL;              // row groups of the transposed staging
-  static constexpr int kRowElems = kTile * RP;
-  static constexpr int kColElems = D * TP;
-  static_assert(NL == 2 || NL == 4, "head_dim 64 or 128");
+  static constexpr int KCH = D / 8;                 // 16-byte chunks per row
+  static constexpr int NL = ROWS * KCH / kThreads;  // chunks per thread
+  static constexpr int kElems = ROWS * D;
+  static_assert(NL == 2 || NL == 4 || NL == 8, "unsupported tile");
 
-  // Row-major: thread t moves chunk t % KCH of tile rows t / KCH + i * (kThreads / KCH).
-  // tab[r] is the tensor row of tile row r, or -1 past the box end (read as zero).
-  // full: every row of the tile lies in the box (no checks, the common case).
-  static __device__ inline void load_rows(uint4 (&r)[NL], const uint16_t* src, const int* tab,
-                                          bool full) {
+  // element offset of (row, channel), channel a multiple of 4
+  static __device__ inline int at(int row, int chan) {
+    const int c = chan >> 3, f = 2 * (row & 3) + ((row >> 2) & 1);
+    return row * D + (((c & ~7) | ((c & 7) ^ f)) << 3) + (chan & 7);
+  }
+
+  // Thread t moves chunk t % KCH of tile rows t / KCH + i * (kThreads / KCH).  tab[r] is the
+  // tensor row of tile row r; `valid` tile rows (those inside the box) are kept, the others
+  // zeroed.  The loads are issued together, without branches.
+  static __device__ inline void load(uint4 (&r)[NL], const uint16_t* src, const int* tab,
+                                     int valid) {
     const int t = threadIdx.x;
+    int row[NL];
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int row = tab[t / KCH + i * (kThreads / KCH)];
-      const uint4* at = reinterpret_cast<const uint4*>(src + (int64_t)row * D + (t % KCH) * 8);
-      if (full) {
-        r[i] = *at;
-      } else {
-        r[i] = make_uint4(0, 0, 0, 0);
-        if (row >= 0) r[i] = *at;
-      }
+    for (int i = 0; i < NL; ++i) row[i] = tab[t / KCH + i * (kThreads / KCH)];
+#pragma unroll
+    for (int i = 0; i < NL; ++i)
+      r[i] = *reinterpret_cast<const uint4*>(src + (int64_t)row[i] * D + (t % KCH) * 8);
+    if (valid < ROWS) {
+#pragma unroll
+      for (int i = 0; i < NL; ++i)
+        if (t / KCH + i * (kThreads / KCH) >= valid) r[i] = make_uint4(0, 0, 0, 0);
     }
   }
-  static __device__ inline void store_rows(uint16_t* lds, const uint4 (&r)[NL]) {
+  static __device__ inline void store(uint16_t* lds, const uint4 (&r)[NL]) {
     const int t = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NL; ++i)
-      *reinterpret_cast<uint4*>(lds + (t / KCH + i * (kThreads / KCH)) * RP + (t % KCH) * 8) = r[i];
+      *reinterpret_cast<uint4*>(lds + at(t / KCH + i * (kThreads / KCH), (t % KCH) * 8)) = r[i];
   }
 
-  // Transposed: thread t moves chunk t / VG of tile rows (t % VG) * NL + e, e < NL, and
-  // writes, for each of the chunk's 8 channels, its NL rows as one 4- or 8-byte word.
-  static __device__ inline void load_cols(uint4 (&r)[NL], const uint16_t* src, const int* tab,
-                                          bool full) {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int e = 0; e < NL; ++e) {
-      const int row = tab[(t % VG) * NL + e];
-      const uint4* at = reinterpret_cast<const uint4*>(src + (int64_t)row * D + (t / VG) * 8);
-      if (full) {
-        r[e] = *at;
-      } else {
-        r[e] = make_uint4(0, 0, 0, 0);
-        if (row >= 0) r[e] = *at;
-      }
-    }
-  }
-  static __device__ inline void store_cols(uint16_t* lds, const uint4 (&r)[NL]) {
-    const int t = threadIdx.x, kg = t % VG, c = t / VG;
-#pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      const bool hi = x & 1;
-      const int w = x >> 1;
-      uint16_t* dst = lds + (c * 8 + x) * TP + kg * NL;
-      const uint32_t w0 = pick_pair(word(r[1], w), word(r[0], w), hi);
-      if constexpr (NL == 4) {
-        const uint32_t w1 = pick_pair(word(r[3], w), word(r[2], w), hi);
-        *reinterpret_cast<uint2*>(dst) = make_uint2(w0, w1);
-      } else {
-        *reinterpret_cast<uint32_t*>(dst) = w0;
-      }
-    }
-  }
-
-  // A operand from a row-major tile: row r0 + l % 32, channels 16 ks + 8 (l / 32) .. +7.
+  // A operand with tile rows as its rows: row r0 + l % 32, channels 16 ks + 8 (l / 32) .. +7.
   static __device__ inline bf16x8_t a_rows(const uint16_t* lds, int r0, int ks) {
     const int lane = threadIdx.x & 63;
-    return as_bf16x8(*reinterpret_cast<const uint4*>(lds + (r0 + (lane & 31)) * RP + ks * 16 +
-                                                     (lane >> 5) * 8));
+    return as_bf16x8(
+        *reinterpret_cast<const uint4*>(lds + at(r0 + (lane & 31), ks * 16 + (lane >> 5) * 8)));
   }
-  // A operand from a transposed tile: channel d0 + l % 32; tile rows 32 kb + 16 p + 4 (l / 32)
+  // A operand with channels as its rows: channel d0 + l % 32; tile rows 32 kb + 16 p + 4 (l / 32)
   // + {0..3, 8..11}, the order in which a C-layout block's elements 8 p .. 8 p + 7 hold them.
+  // ds_read_b64_tr_b16 transposes within each 16-lane group: lane i receives element i % 4 of
+  // the 4-element reads of lanes i / 4 + {0, 4, 8, 12}; so lane j reads 4 channels starting at
+  // c0 + 4 (j % 4) of row base + j / 4, and lane i gets channel c0 + i of rows base .. base + 3.
   static __device__ inline bf16x8_t a_cols(const uint16_t* lds, int d0, int kb, int p) {
-    const int lane = threadIdx.x & 63;
-    const uint16_t* src = lds + (d0 + (lane & 31)) * TP + kb * 32 + 16 * p + 4 * (lane >> 5);
-    const uint2 lo = *reinterpret_cast<const uint2*>(src);
-    const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
-    return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-  }
-
-  static __device__ inline uint32_t word(const uint4& u, int w) {
-    return w == 0 ? u.x : (w == 1 ? u.y : (w == 2 ? u.z : u.w));
+    typedef short s4_t __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s4_t lds_s4_t;
+    const int lane = threadIdx.x & 63, j = lane & 15;
+    const int row = kb * 32 + 16 * p + 4 * (lane >> 5) + (j >> 2);
+    const int chan = d0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+    const uint16_t* src = lds + at(row, chan);
+    const s4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)src);
+    const s4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)(src + 8 * D));
+    const uint2 ul = __builtin_bit_cast(uint2, lo), uh = __builtin_bit_cast(uint2, hi);
+    return as_bf16x8(make_uint4(ul.x, ul.y, uh.x, uh.y));
   }
 };
 
@@ -265,25 +251,29 @@ struct Softmax {
 };
 
 // One workgroup: 128 queries of one (batch, box, head) group against every key of the box,
-// 64 keys per LDS tile, online base-2 softmax.  Wave w owns queries 32 w .. 32 w + 31 of the
+// kFwdTile keys per LDS tile, online base-2 softmax.  Wave w owns queries 32 w .. 32 w + 31 of the
 // tile; lanes l and l ^ 32 share query l % 32 and hold 16 of each 32-key block's logits each.
+// Within a tile the logits of block b + 1 are issued to the matrix cores before the softmax of
+// block b runs on the vector ALUs, so the two overlap.
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                const uint16_t* __restrict__ v, uint16_t* __restrict__ out,
                uint16_t* __restrict__ out_res, float* __restrict__ lse) {
-  using Tl = Tile<D>;
+  constexpr int KT = kFwdTile;
+  using Tl = Tile<D, KT>;
   constexpr int KS = D / 16;  // MFMA k-steps over head_dim
   constexpr int DB = D / 32;  // 32-channel blocks of the output
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kRowElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[Tl::kColElems];
-  __shared__ int tab[2][kTile];  // key rows of the current and the next tile
+  constexpr int NB = KT / 32; // 32-key blocks per tile
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[Tl::kElems];
+  __shared__ int tab[2][KT];  // key rows of the current and the next tile
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int q0 = gr.qt * kQTile, n = gr.bx.n;
   if (q0 >= n) return;  // the box has fewer tiles than the largest one
-  fill_rows(tab[0], g, gr, 0);
+  fill_rows<KT>(tab[0], g, gr, 0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uq = q0 + wave * 32 + (lane & 31);
@@ -297,86 +287,93 @@ win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __
   for (int db = 0; db < DB; ++db) o[db] = f32x16_t{};
   Softmax sm;
 
+  // S^T = K Q^T for 32-key block b of the tile in LDS
+  auto logits = [&](int b) {
+    bf16x8_t a[KS];  // all operands read before the products, so the reads overlap
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) a[ks] = Tl::a_rows(Ks, b * 32, ks);
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16_t acc = f32x16_t{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) acc = mfma(a[ks], qf[ks], acc);
+    return acc;
+  };
+
   uint4 kr[Tl::NL], vr[Tl::NL];
-  const int ntiles = (n + kTile - 1) / kTile;
+  const int ntiles = (n + KT - 1) / KT;
   __syncthreads();
-  Tl::load_rows(kr, k, tab[0], kTile <= n);
-  Tl::load_cols(vr, v, tab[0], kTile <= n);
+  Tl::load(kr, k, tab[0], n);
+  Tl::load(vr, v, tab[0], n);
   for (int kt = 0; kt < ntiles; ++kt) {
-    Tl::store_rows(Ks, kr);
-    Tl::store_cols(Vt, vr);
-    if (kt + 1 < ntiles) fill_rows(tab[(kt + 1) & 1], g, gr, (kt + 1) * kTile);
+    Tl::store(Ks, kr);
+    Tl::store(Vs, vr);
+    if (kt + 1 < ntiles) fill_rows<KT>(tab[(kt + 1) & 1], g, gr, (kt + 1) * KT);
     __syncthreads();
     if (kt + 1 < ntiles) {
-      const bool full = (kt + 2) * kTile <= n;
-      Tl::load_rows(kr, k, tab[(kt + 1) & 1], full);
-      Tl::load_cols(vr, v, tab[(kt + 1) & 1], full);
+      const int valid = n - (kt + 1) * KT;
+      Tl::load(kr, k, tab[(kt + 1) & 1], valid);
+      Tl::load(vr, v, tab[(kt + 1) & 1], valid);
     }
-
-    // S^T = K Q^T for the two 32-key blocks of the tile
-    float s[2][16];
+    const int kbase = kt * KT;
+    const int nb = min(NB, (n - kbase + 31) / 32);  // blocks holding at least one key
+    f32x16_t cur = logits(0);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16_t acc = f32x16_t{};
+    for (int b = 0; b < NB; ++b) {
+      if (b >= nb) break;
+      f32x16_t nxt;
+      if (b + 1 < nb) nxt = logits(b + 1);
+      // V^T operands of this block, read now so that the softmax below hides their latency
+      bf16x8_t av[DB][2];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc = mfma(Tl::a_rows(Ks, kb * 32, ks), qf[ks], acc);
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s[kb][i] = acc[i];
-    }
-    const int kbase = kt * kTile;
-    if (kbase + kTile > n) {  // ragged last tile: keys past the box end get -inf
+        for (int p = 0; p < 2; ++p) av[db][p] = Tl::a_cols(Vs, db * 32, b, p);
+      float s[16];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int i = 0; i < 16; ++i) s[i] = cur[i];
+      if (kbase + b * 32 + 32 > n) {  // ragged block: keys past the box end get -inf
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          if (kbase + kb * 32 + 8 * (i / 4) + 4 * hh + (i % 4) >= n) s[kb][i] = -INFINITY;
-    }
-    float mx = s[0][0];
+          if (kbase + b * 32 + 8 * (i / 4) + 4 * hh + (i % 4) >= n) s[i] = -INFINITY;
+      }
+      float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int i = 3; i < 16; ++i) mx = fmaxf(mx, s[i]);
+      mx = pair_max(mx) * g.scale_log2;  // scale > 0
+      // The running maximum is raised only when a logit exceeds it by more than kSlack
+      // (base 2), so P stays below 2^kSlack and the rescale of O is skipped by whole waves
+      // most of the time; the result does not depend on which maximum was used.
+      const bool raise = mx > sm.m + kSlack;
+      if (__any(raise)) {
+        const float mnew = raise ? mx : sm.m;
+        const float corr = __builtin_amdgcn_exp2f(sm.m - mnew);
+        sm.m = mnew;
+        sm.l *= corr;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * g.scale_log2;  // scale > 0
-    // The running maximum is raised only when a logit exceeds it by more than kSlack (base 2),
-    // so P stays below 2^kSlack and the rescale of O is skipped by whole waves most of the
-    // time; the result does not depend on which maximum was used.
-    const bool raise = mx > sm.m + kSlack;
-    if (__any(raise)) {
-      const float mnew = raise ? mx : sm.m;
-      const float corr = __builtin_amdgcn_exp2f(sm.m - mnew);
-      sm.m = mnew;
-      sm.l *= corr;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[db] *= corr;
-    }
-    const float mnew = sm.m;
-
-    bf16x8_t ph[2][2], pl[2][2];  // P^T as B-operand fragments (hi + lo)
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+        for (int db = 0; db < DB; ++db) o[db] *= corr;
+      }
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        s[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[kb][i], g.scale_log2, -mnew));
-        sm.l += s[kb][i];
+        s[i] = __builtin_amdgcn_exp2f(fmaf(s[i], g.scale_log2, -sm.m));
+        sm.l += s[i];
       }
-      to_frags(s[kb], ph[kb], pl[kb]);
-    }
-
-    // O^T += V^T P^T
+      bf16x8_t ph[2], pl[2];  // P^T as B-operand fragments (hi + lo)
+      to_frags(s, ph, pl);
+      // O^T += V^T P^T
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
-          const bf16x8_t a = Tl::a_cols(Vt, db * 32, kb, p);
-          o[db] = mfma(a, ph[kb][p], o[db]);
-          o[db] = mfma(a, pl[kb][p], o[db]);
+          o[db] = mfma(av[db][p], ph[p], o[db]);
+          o[db] = mfma(av[db][p], pl[p], o[db]);
         }
+      cur = nxt;
+    }
     __syncthreads();
   }
 
-  const float ltot = sm.l + __shfl_xor(sm.l, 32);
+  const float ltot = pair_sum(sm.l);
   if (!qok) return;
   const float inv = 1.0f / ltot;
   const int64_t obase = qrow * D + 4 * hh;
@@ -412,18 +409,17 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
               const uint16_t* __restrict__ out_res, const float* __restrict__ lse,
               const uint16_t* __restrict__ dout, float* __restrict__ dq,
               float* __restrict__ delta) {
-  using Tl = Tile<D>;
+  using Tl = Tile<D, kTile>;
   constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kRowElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[Tl::kRowElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Kt[Tl::kColElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[Tl::kElems];
   __shared__ int tab[2][kTile];  // key rows of the current and the next tile
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int q0 = gr.qt * kQTile, n = gr.bx.n;
   if (q0 >= n) return;
-  fill_rows(tab[0], g, gr, 0);
+  fill_rows<kTile>(tab[0], g, gr, 0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uq = q0 + wave * 32 + (lane & 31);
@@ -443,7 +439,7 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         part = fmaf((float)gf[ks][e], (float)of[ks][e] + (float)rf[ks][e], part);
-    dl = part + __shfl_xor(part, 32);
+    dl = pair_sum(part);
   }
   if (qok && hh == 0) delta[qrow] = dl;
   const float lse2 = qok ? lse[qrow] * 1.4426950408889634f : 0.0f;
@@ -452,24 +448,21 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16_t{};
 
-  uint4 kr[Tl::NL], vr[Tl::NL], kc[Tl::NL];
+  uint4 kr[Tl::NL], vr[Tl::NL];
   const int ntiles = (n + kTile - 1) / kTile;
   __syncthreads();
-  Tl::load_rows(kr, k, tab[0], kTile <= n);
-  Tl::load_rows(vr, v, tab[0], kTile <= n);
-  Tl::load_cols(kc, k, tab[0], kTile <= n);
+  Tl::load(kr, k, tab[0], n);
+  Tl::load(vr, v, tab[0], n);
   for (int kt = 0; kt < ntiles; ++kt) {
-    Tl::store_rows(Ks, kr);
-    Tl::store_rows(Vs, vr);
-    Tl::store_cols(Kt, kc);
-    if (kt + 1 < ntiles) fill_rows(tab[(kt + 1) & 1], g, gr, (kt + 1) * kTile);
+    Tl::store(Ks, kr);
+    Tl::store(Vs, vr);
+    if (kt + 1 < ntiles) fill_rows<kTile>(tab[(kt + 1) & 1], g, gr, (kt + 1) * kTile);
     __syncthreads();
     if (kt + 1 < ntiles) {
       const int* t1 = tab[(kt + 1) & 1];
-      const bool full = (kt + 2) * kTile <= n;
-      Tl::load_rows(kr, k, t1, full);
-      Tl::load_rows(vr, v, t1, full);
-      Tl::load_cols(kc, k, t1, full);
+      const int valid = n - (kt + 1) * kTile;
+      Tl::load(kr, k, t1, valid);
+      Tl::load(vr, v, t1, valid);
     }
     const int kbase = kt * kTile;
 #pragma unroll
@@ -493,7 +486,7 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
-          const bf16x8_t a = Tl::a_cols(Kt, db * 32, kb, p);
+          const bf16x8_t a = Tl::a_cols(Ks, db * 32, kb, p);
           acc[db] = mfma(a, dh[p], acc[db]);
           acc[db] = mfma(a, dlo[p], acc[db]);
         }
@@ -510,17 +503,15 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
 //   S = Q K^T,  P = exp2(s log2(e) scale - lse log2(e)),  dP = dout V^T,  dS = P (dP - Delta),
 //   dv^T += dout^T P,  dk^T += Q^T dS  (scaled by `scale` at the end).
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(D == 128 ? 1 : 2, 2))) void
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 2))) void
 win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, const float* __restrict__ lse,
                 const uint16_t* __restrict__ dout, const float* __restrict__ delta,
                 float* __restrict__ dk, float* __restrict__ dv) {
-  using Tl = Tile<D>;
+  using Tl = Tile<D, kTile>;
   constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[Tl::kRowElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Gs[Tl::kRowElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[Tl::kColElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Gt[Tl::kColElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[Tl::kElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Gs[Tl::kElems];
   __shared__ __attribute__((aligned(16))) float Ls[kTile];  // lse log2(e); +inf past the box end
   __shared__ __attribute__((aligned(16))) float Dl[kTile];  // Delta
   __shared__ int tab[2][kTile];  // query rows of the current and the next tile
@@ -529,7 +520,7 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
   if (!group_of(g, g.qtiles, gr)) return;
   const int k0 = gr.qt * kQTile, n = gr.bx.n;
   if (k0 >= n) return;
-  fill_rows(tab[0], g, gr, 0);
+  fill_rows<kTile>(tab[0], g, gr, 0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uk = k0 + wave * 32 + (lane & 31);
@@ -544,73 +535,97 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
   for (int db = 0; db < DB; ++db) dka[db] = dva[db] = f32x16_t{};
 
   // the next query tile is fetched into registers while the current one is used
-  uint4 rq[Tl::NL], cq[Tl::NL], rg[Tl::NL], cg[Tl::NL];
+  uint4 rq[Tl::NL], rg[Tl::NL];
   float ls = INFINITY, de = 0.0f;
-  auto fetch = [&](const int* t1, bool full) {
-    Tl::load_rows(rq, q, t1, full);
-    Tl::load_cols(cq, q, t1, full);
-    Tl::load_rows(rg, dout, t1, full);
-    Tl::load_cols(cg, dout, t1, full);
+  auto fetch = [&](const int* t1, int valid) {
+    Tl::load(rq, q, t1, valid);
+    Tl::load(rg, dout, t1, valid);
     if (threadIdx.x < kTile) {
       const int row = t1[threadIdx.x];
-      ls = INFINITY;
-      de = 0.0f;
-      if (row >= 0) {
-        ls = lse[row] * 1.4426950408889634f;
-        de = delta[row];
-      }
+      const bool ok = (int)threadIdx.x < valid;
+      ls = ok ? lse[row] * 1.4426950408889634f : INFINITY;
+      de = ok ? delta[row] : 0.0f;
     }
   };
   const int ntiles = (n + kTile - 1) / kTile;
   __syncthreads();
-  fetch(tab[0], kTile <= n);
+  fetch(tab[0], n);
   for (int qt = 0; qt < ntiles; ++qt) {
-    Tl::store_rows(Qs, rq);
-    Tl::store_cols(Qt, cq);
-    Tl::store_rows(Gs, rg);
-    Tl::store_cols(Gt, cg);
+    Tl::store(Qs, rq);
+    Tl::store(Gs, rg);
     if (threadIdx.x < kTile) {
       Ls[threadIdx.x] = ls;
       Dl[threadIdx.x] = de;
     }
-    if (qt + 1 < ntiles) fill_rows(tab[(qt + 1) & 1], g, gr, (qt + 1) * kTile);
+    if (qt + 1 < ntiles) fill_rows<kTile>(tab[(qt + 1) & 1], g, gr, (qt + 1) * kTile);
     __syncthreads();
-    if (qt + 1 < ntiles) fetch(tab[(qt + 1) & 1], (qt + 2) * kTile <= n);
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      f32x16_t sa = f32x16_t{}, pa = f32x16_t{};
+    if (qt + 1 < ntiles) fetch(tab[(qt + 1) & 1], n - (qt + 1) * kTile);
+    // S and dP of 32-query block qb: operands read together, then the products
+    auto sdp = [&](int qb, f32x16_t& sa, f32x16_t& pa) {
+      bf16x8_t aq[KS], ag[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        sa = mfma(Tl::a_rows(Qs, qb * 32, ks), kf[ks], sa);
-        pa = mfma(Tl::a_rows(Gs, qb * 32, ks), vf[ks], pa);
+        aq[ks] = Tl::a_rows(Qs, qb * 32, ks);
+        ag[ks] = Tl::a_rows(Gs, qb * 32, ks);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      sa = f32x16_t{};
+      pa = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        sa = mfma(aq[ks], kf[ks], sa);
+        pa = mfma(ag[ks], vf[ks], pa);
+      }
+    };
+    f32x16_t sc, pc;
+    sdp(0, sc, pc);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      // the next block's products go to the matrix cores before this block's softmax
+      f32x16_t sn, pn;
+      if (qb == 0) sdp(1, sn, pn);
+      // dV and dK operands and the queries' lse and Delta, read before the vector work
+      bf16x8_t ag[DB][2], aq[DB][2];
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+          ag[db][pp] = Tl::a_cols(Gs, db * 32, qb, pp);
+          aq[db][pp] = Tl::a_cols(Qs, db * 32, qb, pp);
+        }
+      float4 l4[4], d4[4];
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) {
+        l4[blk] = *reinterpret_cast<const float4*>(Ls + qb * 32 + 8 * blk + 4 * hh);
+        d4[blk] = *reinterpret_cast<const float4*>(Dl + qb * 32 + 8 * blk + 4 * hh);
       }
       float p[16], ds[16];
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) {
-        const float4 l4 = *reinterpret_cast<const float4*>(Ls + qb * 32 + 8 * blk + 4 * hh);
-        const float4 d4 = *reinterpret_cast<const float4*>(Dl + qb * 32 + 8 * blk + 4 * hh);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+        const float lv[4] = {l4[blk].x, l4[blk].y, l4[blk].z, l4[blk].w};
+        const float dv4[4] = {d4[blk].x, d4[blk].y, d4[blk].z, d4[blk].w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int i = 4 * blk + j;
-          p[i] = __builtin_amdgcn_exp2f(fmaf(sa[i], g.scale_log2, -lv[j]));
-          ds[i] = p[i] * (pa[i] - dv4[j]);
+          p[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], g.scale_log2, -lv[j]));
+          ds[i] = p[i] * (pc[i] - dv4[j]);
         }
       }
       bf16x8_t ph[2], pl[2], dh[2], dlo[2];
       to_frags(p, ph, pl);
       to_frags(ds, dh, dlo);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp) {
-          const bf16x8_t ag = Tl::a_cols(Gt, db * 32, qb, pp);
-          dva[db] = mfma(ag, ph[pp], dva[db]);
-          dva[db] = mfma(ag, pl[pp], dva[db]);
-          const bf16x8_t aq = Tl::a_cols(Qt, db * 32, qb, pp);
-          dka[db] = mfma(aq, dh[pp], dka[db]);
-          dka[db] = mfma(aq, dlo[pp], dka[db]);
+          dva[db] = mfma(ag[db][pp], ph[pp], dva[db]);
+          dva[db] = mfma(ag[db][pp], pl[pp], dva[db]);
+          dka[db] = mfma(aq[db][pp], dh[pp], dka[db]);
+          dka[db] = mfma(aq[db][pp], dlo[pp], dka[db]);
         }
+      sc = sn;
+      pc = pn;
     }
     __syncthreads();
   }
