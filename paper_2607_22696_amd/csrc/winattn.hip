@@ -128,11 +128,13 @@ __device__ inline void fill_rows(int* tab, const WinGeometry& g, const Group& gr
 
 // A tile of ROWS box rows (box-local indices base .. base + ROWS - 1; rows past the box end
 // read as zero) of a [rows][D] bf16 tensor in LDS, gathered through the box's token order.
-// Rows are D channels long, unpadded; within each run of 8 16-byte chunks of a row the chunks
-// are XOR-permuted by f(row) = 2 (row % 4) + (row / 4) % 2.  Then 16-byte reads of one chunk
-// of 8 consecutive rows (the row-major operand) and the transposing 8-byte reads of 4
-// consecutive rows x 32 bytes (the column operand) both hit every bank once.  Each thread
-// stages NL 16-byte chunks.
+// Rows are D channels long, unpadded, and the 16-byte chunks of a row are XOR-permuted by a
+// function of the row so that both operand reads cover the 256 bytes the LDS serves per
+// cycle without a repeated bank: the 16-byte reads of one chunk of 16 consecutive rows (the
+// row-major operand) and the transposing 8-byte reads of 4 consecutive rows x 64 bytes (the
+// column operand).  D = 128 (16 chunks, one row per 256 bytes): f = 4 (row % 4) + (row / 4) % 4;
+// D = 64 (8 chunks, the row's parity picks the 128-byte half):
+// f = 4 ((row / 2) % 2) + (row / 4) % 4.  Each thread stages NL 16-byte chunks.
 template <int D, int ROWS>
 struct Tile {
   static constexpr int KCH = D / 8;                 // 16-byte chunks per row
@@ -142,8 +144,10 @@ struct Tile {
 
   // element offset of (row, channel), channel a multiple of 4
   static __device__ inline int at(int row, int chan) {
-    const int c = chan >> 3, f = 2 * (row & 3) + ((row >> 2) & 1);
-    return row * D + (((c & ~7) | ((c & 7) ^ f)) << 3) + (chan & 7);
+    static_assert(D == 64 || D == 128, "head_dim 64 or 128");
+    const int f = D == 128 ? 4 * (row & 3) + ((row >> 2) & 3)
+                           : 4 * ((row >> 1) & 1) + ((row >> 2) & 3);
+    return row * D + (((chan >> 3) ^ f) << 3) + (chan & 7);
   }
 
   // Thread t moves chunk t % KCH of tile rows t / KCH + i * (kThreads / KCH).  tab[r] is the
@@ -188,9 +192,8 @@ struct Tile {
     const int lane = threadIdx.x & 63, j = lane & 15;
     const int row = kb * 32 + 16 * p + 4 * (lane >> 5) + (j >> 2);
     const int chan = d0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
-    const uint16_t* src = lds + at(row, chan);
-    const s4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)src);
-    const s4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)(src + 8 * D));
+    const s4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)(lds + at(row, chan)));
+    const s4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4_t*)(lds + at(row + 8, chan)));
     const uint2 ul = __builtin_bit_cast(uint2, lo), uh = __builtin_bit_cast(uint2, hi);
     return as_bf16x8(make_uint4(ul.x, ul.y, uh.x, uh.y));
   }
@@ -265,15 +268,16 @@ win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __
   constexpr int KS = D / 16;  // MFMA k-steps over head_dim
   constexpr int DB = D / 32;  // 32-channel blocks of the output
   constexpr int NB = KT / 32; // 32-key blocks per tile
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[Tl::kElems];
-  __shared__ int tab[2][KT];  // key rows of the current and the next tile
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][Tl::kElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][Tl::kElems];
+  __shared__ int tab[3][KT];  // key rows of tile i in slot i % 3
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int q0 = gr.qt * kQTile, n = gr.bx.n;
   if (q0 >= n) return;  // the box has fewer tiles than the largest one
-  fill_rows<KT>(tab[0], g, gr, 0);
+  const int ntiles = (n + KT - 1) / KT;
+  for (int i = 0; i < 3 && i < ntiles; ++i) fill_rows<KT>(tab[i], g, gr, i * KT);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uq = q0 + wave * 32 + (lane & 31);
@@ -287,11 +291,11 @@ win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __
   for (int db = 0; db < DB; ++db) o[db] = f32x16_t{};
   Softmax sm;
 
-  // S^T = K Q^T for 32-key block b of the tile in LDS
-  auto logits = [&](int b) {
+  // S^T = K Q^T for 32-key block b of the tile in LDS buffer kb
+  auto logits = [&](const uint16_t* kb, int b) {
     bf16x8_t a[KS];  // all operands read before the products, so the reads overlap
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) a[ks] = Tl::a_rows(Ks, b * 32, ks);
+    for (int ks = 0; ks < KS; ++ks) a[ks] = Tl::a_rows(kb, b * 32, ks);
     __builtin_amdgcn_sched_barrier(0);
     f32x16_t acc = f32x16_t{};
 #pragma unroll
@@ -299,35 +303,47 @@ win_fwd_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __
     return acc;
   };
 
+  // Tile i is staged in LDS buffer i & 1; its global loads go out one tile ahead and its row
+  // table is filled three tiles ahead.  One barrier per tile: a buffer or table slot is
+  // rewritten only after the barrier that follows its last read, and read only after the
+  // barrier that follows its write.
   uint4 kr[Tl::NL], vr[Tl::NL];
-  const int ntiles = (n + KT - 1) / KT;
   __syncthreads();
   Tl::load(kr, k, tab[0], n);
   Tl::load(vr, v, tab[0], n);
+  Tl::store(Ks[0], kr);
+  Tl::store(Vs[0], vr);
+  if (ntiles > 1) {
+    Tl::load(kr, k, tab[1], n - KT);
+    Tl::load(vr, v, tab[1], n - KT);
+  }
+  __syncthreads();
   for (int kt = 0; kt < ntiles; ++kt) {
-    Tl::store(Ks, kr);
-    Tl::store(Vs, vr);
-    if (kt + 1 < ntiles) fill_rows<KT>(tab[(kt + 1) & 1], g, gr, (kt + 1) * KT);
-    __syncthreads();
+    const uint16_t *kc = Ks[kt & 1], *vc = Vs[kt & 1];
     if (kt + 1 < ntiles) {
-      const int valid = n - (kt + 1) * KT;
-      Tl::load(kr, k, tab[(kt + 1) & 1], valid);
-      Tl::load(vr, v, tab[(kt + 1) & 1], valid);
+      Tl::store(Ks[(kt + 1) & 1], kr);
+      Tl::store(Vs[(kt + 1) & 1], vr);
     }
+    if (kt + 2 < ntiles) {
+      const int* t2 = tab[(kt + 2) % 3];
+      Tl::load(kr, k, t2, n - (kt + 2) * KT);
+      Tl::load(vr, v, t2, n - (kt + 2) * KT);
+    }
+    if (kt + 3 < ntiles) fill_rows<KT>(tab[kt % 3], g, gr, (kt + 3) * KT);
     const int kbase = kt * KT;
     const int nb = min(NB, (n - kbase + 31) / 32);  // blocks holding at least one key
-    f32x16_t cur = logits(0);
+    f32x16_t cur = logits(kc, 0);
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       if (b >= nb) break;
       f32x16_t nxt;
-      if (b + 1 < nb) nxt = logits(b + 1);
+      if (b + 1 < nb) nxt = logits(kc, b + 1);
       // V^T operands of this block, read now so that the softmax below hides their latency
       bf16x8_t av[DB][2];
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int p = 0; p < 2; ++p) av[db][p] = Tl::a_cols(Vs, db * 32, b, p);
+        for (int p = 0; p < 2; ++p) av[db][p] = Tl::a_cols(vc, db * 32, b, p);
       float s[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[i] = cur[i];
@@ -411,15 +427,16 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
               float* __restrict__ delta) {
   using Tl = Tile<D, kTile>;
   constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[Tl::kElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[Tl::kElems];
-  __shared__ int tab[2][kTile];  // key rows of the current and the next tile
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][Tl::kElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][Tl::kElems];
+  __shared__ int tab[3][kTile];  // key rows of tile i in slot i % 3
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int q0 = gr.qt * kQTile, n = gr.bx.n;
   if (q0 >= n) return;
-  fill_rows<kTile>(tab[0], g, gr, 0);
+  const int ntiles = (n + kTile - 1) / kTile;
+  for (int i = 0; i < 3 && i < ntiles; ++i) fill_rows<kTile>(tab[i], g, gr, i * kTile);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uq = q0 + wave * 32 + (lane & 31);
@@ -448,37 +465,50 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x16_t{};
 
+  // staging as in the forward: tile i in LDS buffer i & 1, loads one tile ahead, row table
+  // three tiles ahead, one barrier per tile
   uint4 kr[Tl::NL], vr[Tl::NL];
-  const int ntiles = (n + kTile - 1) / kTile;
   __syncthreads();
   Tl::load(kr, k, tab[0], n);
   Tl::load(vr, v, tab[0], n);
+  Tl::store(Ks[0], kr);
+  Tl::store(Vs[0], vr);
+  if (ntiles > 1) {
+    Tl::load(kr, k, tab[1], n - kTile);
+    Tl::load(vr, v, tab[1], n - kTile);
+  }
+  __syncthreads();
   for (int kt = 0; kt < ntiles; ++kt) {
-    Tl::store(Ks, kr);
-    Tl::store(Vs, vr);
-    if (kt + 1 < ntiles) fill_rows<kTile>(tab[(kt + 1) & 1], g, gr, (kt + 1) * kTile);
-    __syncthreads();
+    const uint16_t *kc = Ks[kt & 1], *vc = Vs[kt & 1];
     if (kt + 1 < ntiles) {
-      const int* t1 = tab[(kt + 1) & 1];
-      const int valid = n - (kt + 1) * kTile;
-      Tl::load(kr, k, t1, valid);
-      Tl::load(vr, v, t1, valid);
+      Tl::store(Ks[(kt + 1) & 1], kr);
+      Tl::store(Vs[(kt + 1) & 1], vr);
     }
+    if (kt + 2 < ntiles) {
+      const int* t2 = tab[(kt + 2) % 3];
+      Tl::load(kr, k, t2, n - (kt + 2) * kTile);
+      Tl::load(vr, v, t2, n - (kt + 2) * kTile);
+    }
+    if (kt + 3 < ntiles) fill_rows<kTile>(tab[kt % 3], g, gr, (kt + 3) * kTile);
     const int kbase = kt * kTile;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x16_t sa = f32x16_t{}, pa = f32x16_t{};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        sa = mfma(Tl::a_rows(Ks, kb * 32, ks), qf[ks], sa);
-        pa = mfma(Tl::a_rows(Vs, kb * 32, ks), gf[ks], pa);
+        sa = mfma(Tl::a_rows(kc, kb * 32, ks), qf[ks], sa);
+        pa = mfma(Tl::a_rows(vc, kb * 32, ks), gf[ks], pa);
       }
       float ds[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const bool ok = kbase + kb * 32 + 8 * (i / 4) + 4 * hh + (i % 4) < n;
-        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(sa[i], g.scale_log2, -lse2)) : 0.0f;
+        const float p = __builtin_amdgcn_exp2f(fmaf(sa[i], g.scale_log2, -lse2));
         ds[i] = p * (pa[i] - dl);
+      }
+      if (kbase + kb * 32 + 32 > n) {  // ragged block: keys past the box end contribute nothing
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (kbase + kb * 32 + 8 * (i / 4) + 4 * hh + (i % 4) >= n) ds[i] = 0.0f;
       }
       bf16x8_t dh[2], dlo[2];
       to_frags(ds, dh, dlo);
@@ -486,7 +516,7 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
-          const bf16x8_t a = Tl::a_cols(Ks, db * 32, kb, p);
+          const bf16x8_t a = Tl::a_cols(kc, db * 32, kb, p);
           acc[db] = mfma(a, dh[p], acc[db]);
           acc[db] = mfma(a, dlo[p], acc[db]);
         }
@@ -510,17 +540,18 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
                 float* __restrict__ dk, float* __restrict__ dv) {
   using Tl = Tile<D, kTile>;
   constexpr int KS = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[Tl::kElems];
-  __shared__ __attribute__((aligned(16))) uint16_t Gs[Tl::kElems];
-  __shared__ __attribute__((aligned(16))) float Ls[kTile];  // lse log2(e); +inf past the box end
-  __shared__ __attribute__((aligned(16))) float Dl[kTile];  // Delta
-  __shared__ int tab[2][kTile];  // query rows of the current and the next tile
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[2][Tl::kElems];
+  __shared__ __attribute__((aligned(16))) uint16_t Gs[2][Tl::kElems];
+  __shared__ __attribute__((aligned(16))) float Ls[2][kTile];  // lse log2(e); +inf past the end
+  __shared__ __attribute__((aligned(16))) float Dl[2][kTile];  // Delta
+  __shared__ int tab[3][kTile];  // query rows of tile i in slot i % 3
 
   Group gr;
   if (!group_of(g, g.qtiles, gr)) return;
   const int k0 = gr.qt * kQTile, n = gr.bx.n;
   if (k0 >= n) return;
-  fill_rows<kTile>(tab[0], g, gr, 0);
+  const int ntiles = (n + kTile - 1) / kTile;
+  for (int i = 0; i < 3 && i < ntiles; ++i) fill_rows<kTile>(tab[i], g, gr, i * kTile);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
   const int uk = k0 + wave * 32 + (lane & 31);
@@ -534,7 +565,8 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
 #pragma unroll
   for (int db = 0; db < DB; ++db) dka[db] = dva[db] = f32x16_t{};
 
-  // the next query tile is fetched into registers while the current one is used
+  // staging as in the forward: query tile i (q, dout, and the queries' lse and Delta) in LDS
+  // buffer i & 1, loads one tile ahead, row table three tiles ahead, one barrier per tile
   uint4 rq[Tl::NL], rg[Tl::NL];
   float ls = INFINITY, de = 0.0f;
   auto fetch = [&](const int* t1, int valid) {
@@ -547,26 +579,32 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
       de = ok ? delta[row] : 0.0f;
     }
   };
-  const int ntiles = (n + kTile - 1) / kTile;
+  auto stage = [&](int buf) {
+    Tl::store(Qs[buf], rq);
+    Tl::store(Gs[buf], rg);
+    if (threadIdx.x < kTile) {
+      Ls[buf][threadIdx.x] = ls;
+      Dl[buf][threadIdx.x] = de;
+    }
+  };
   __syncthreads();
   fetch(tab[0], n);
+  stage(0);
+  if (ntiles > 1) fetch(tab[1], n - kTile);
+  __syncthreads();
   for (int qt = 0; qt < ntiles; ++qt) {
-    Tl::store(Qs, rq);
-    Tl::store(Gs, rg);
-    if (threadIdx.x < kTile) {
-      Ls[threadIdx.x] = ls;
-      Dl[threadIdx.x] = de;
-    }
-    if (qt + 1 < ntiles) fill_rows<kTile>(tab[(qt + 1) & 1], g, gr, (qt + 1) * kTile);
-    __syncthreads();
-    if (qt + 1 < ntiles) fetch(tab[(qt + 1) & 1], n - (qt + 1) * kTile);
+    const uint16_t *Qc = Qs[qt & 1], *Gc = Gs[qt & 1];
+    const float *Lc = Ls[qt & 1], *Dc = Dl[qt & 1];
+    if (qt + 1 < ntiles) stage((qt + 1) & 1);
+    if (qt + 2 < ntiles) fetch(tab[(qt + 2) % 3], n - (qt + 2) * kTile);
+    if (qt + 3 < ntiles) fill_rows<kTile>(tab[qt % 3], g, gr, (qt + 3) * kTile);
     // S and dP of 32-query block qb: operands read together, then the products
     auto sdp = [&](int qb, f32x16_t& sa, f32x16_t& pa) {
       bf16x8_t aq[KS], ag[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        aq[ks] = Tl::a_rows(Qs, qb * 32, ks);
-        ag[ks] = Tl::a_rows(Gs, qb * 32, ks);
+        aq[ks] = Tl::a_rows(Qc, qb * 32, ks);
+        ag[ks] = Tl::a_rows(Gc, qb * 32, ks);
       }
       __builtin_amdgcn_sched_barrier(0);
       sa = f32x16_t{};
@@ -584,26 +622,12 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
       // the next block's products go to the matrix cores before this block's softmax
       f32x16_t sn, pn;
       if (qb == 0) sdp(1, sn, pn);
-      // dV and dK operands and the queries' lse and Delta, read before the vector work
-      bf16x8_t ag[DB][2], aq[DB][2];
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int pp = 0; pp < 2; ++pp) {
-          ag[db][pp] = Tl::a_cols(Gs, db * 32, qb, pp);
-          aq[db][pp] = Tl::a_cols(Qs, db * 32, qb, pp);
-        }
-      float4 l4[4], d4[4];
-#pragma unroll
-      for (int blk = 0; blk < 4; ++blk) {
-        l4[blk] = *reinterpret_cast<const float4*>(Ls + qb * 32 + 8 * blk + 4 * hh);
-        d4[blk] = *reinterpret_cast<const float4*>(Dl + qb * 32 + 8 * blk + 4 * hh);
-      }
       float p[16], ds[16];
 #pragma unroll
-      for (int blk = 0; blk < 4; ++blk) {
-        const float lv[4] = {l4[blk].x, l4[blk].y, l4[blk].z, l4[blk].w};
-        const float dv4[4] = {d4[blk].x, d4[blk].y, d4[blk].z, d4[blk].w};
+      for (int blk = 0; blk < 4; ++blk) {  // the queries' lse and Delta
+        const float4 l4 = *reinterpret_cast<const float4*>(Lc + qb * 32 + 8 * blk + 4 * hh);
+        const float4 d4 = *reinterpret_cast<const float4*>(Dc + qb * 32 + 8 * blk + 4 * hh);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv4[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int i = 4 * blk + j;
@@ -614,15 +638,16 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
       bf16x8_t ph[2], pl[2], dh[2], dlo[2];
       to_frags(p, ph, pl);
       to_frags(ds, dh, dlo);
-      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp) {
-          dva[db] = mfma(ag[db][pp], ph[pp], dva[db]);
-          dva[db] = mfma(ag[db][pp], pl[pp], dva[db]);
-          dka[db] = mfma(aq[db][pp], dh[pp], dka[db]);
-          dka[db] = mfma(aq[db][pp], dlo[pp], dka[db]);
+          const bf16x8_t ag = Tl::a_cols(Gc, db * 32, qb, pp);
+          const bf16x8_t aq = Tl::a_cols(Qc, db * 32, qb, pp);
+          dva[db] = mfma(ag, ph[pp], dva[db]);
+          dva[db] = mfma(ag, pl[pp], dva[db]);
+          dka[db] = mfma(aq, dh[pp], dka[db]);
+          dka[db] = mfma(aq, dlo[pp], dka[db]);
         }
       sc = sn;
       pc = pn;
