@@ -153,6 +153,47 @@ def algorithmic(w):
     return {k: {"bytes": rows * b, "flops": rows * f} for k, (b, f) in per.items()}
 
 
+def vmem_bytes(w):
+    """Bytes that the vector-memory instructions (loads and stores through each compute
+    unit's L1 path) of the query-owned kernels move per launch, per query row (s = bytes per
+    q/k/v element):
+      fwd_kernel           16 P D s (8 K and 8 V corner rows per point) + D s (q) + 12 P
+                           (offsets) + D s (out) + 4 (lse)
+      bwd_sweep_kernel     16 P D s + 2 D s (q, dout) + 12 P + 4 (lse) + 32 P (point records)
+                           + 4 P (bin-count atomics) + 4 D (dq) + 4 (Delta)
+      bwd_finalize_kernel  32 P (records) + 4 P (Delta) + 12 P (offsets) + 12 P (d_offsets)
+                           + 4 P (slot atomic) + 24 P (bin entry)
+    These, not the HBM bytes, are what bounds the kernels: the corner rows come from L2 and
+    L1, and the per-unit gather path is busy ~90% of the time (rocprofv3 TA/TD counters)."""
+    s = 2 if w.dtype == "bf16" else 4
+    P, D = w.P, w.head_dim
+    per = {
+        "fwd_kernel": 16 * P * D * s + 2 * D * s + 12 * P + 4,
+        "bwd_sweep_kernel": 16 * P * D * s + 2 * D * s + 12 * P + 4 + 36 * P + 4 * D + 4,
+        "bwd_finalize_kernel": 88 * P,
+    }
+    return {k: w.queries * b for k, b in per.items()}
+
+
+def gather_ceiling(row_bytes):
+    """The gather microbenchmark (libdsa3d_probe.so): 16-byte lane loads, one contiguous row
+    of row_bytes per lane group at pseudo-random addresses, every row already in L1 (the
+    ceiling of the kernels' gather path), and the same pattern from LDS."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_22696_amd", "libdsa3d_probe.so"))
+    lib.dsa3d_probe_gather.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.POINTER(ctypes.c_float),
+                                       ctypes.POINTER(ctypes.c_double)]
+    out = {"row_bytes": row_bytes}
+    for src, name in ((0, "l1"), (1, "lds")):
+        ms, nb = ctypes.c_float(), ctypes.c_double()
+        rc = lib.dsa3d_probe_gather(src, row_bytes, 2048, 4096, ctypes.byref(ms), ctypes.byref(nb))
+        if rc != 0:
+            raise RuntimeError(f"gather probe failed ({rc})")
+        out[f"{name}_TBps"] = round(nb.value / (ms.value * 1e-3) / 1e12, 2)
+    return out
+
+
 def roofline(work, ms):
     """Roofline entry of one kernel: bound by whichever of HBM bytes and fp32 VALU flops takes
     longer at peak; achieved = algorithmic work per launch / average launch time."""
@@ -719,6 +760,16 @@ def main():
     roof["kernel"] = kname
     roof["avg_launch_ms"] = round(kernel_ms[kname], 4)
 
+    # the bound the kernels actually meet: bytes through the per-unit vector-memory path
+    ceil = gather_ceiling(w.head_dim * (2 if w.dtype == "bf16" else 4))
+    vm = vmem_bytes(w)
+    gather_path = {"ceiling": ceil}
+    for n, b in vm.items():
+        if n in kernel_ms:
+            tbps = b / (kernel_ms[n] * 1e-3) / 1e12
+            gather_path[n] = {"bytes_per_launch": b, "achieved_TBps": round(tbps, 2),
+                              "frac_of_l1_ceiling": round(tbps / ceil["l1_TBps"], 3)}
+
     res = {
         "metric": METRIC,
         "value": round(tokens / (ms_step * 1e-3), 1),
@@ -743,6 +794,7 @@ def main():
         "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "token_head_rows_per_s": round(w.queries / (ms_step * 1e-3), 1),
         "roofline": roof,
+        "gather_path": gather_path,
         "input_gen_s": round(t_gen, 1),
     }
     if args.cpu_budget > 0:

@@ -1,4 +1,5 @@
-"""Builds libdsa3d.so (gfx950 HIP kernels + C-ABI host code) in-tree with hipcc."""
+"""Builds libdsa3d.so (gfx950 HIP kernels + C-ABI host code) in-tree with hipcc, and the
+gather-bandwidth microbenchmark libdsa3d_probe.so that bench.py uses for its ceiling."""
 from __future__ import annotations
 
 import os
@@ -10,6 +11,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdsa3d.so")
+PROBE_LIB = os.path.join(PKG, "libdsa3d_probe.so")
+PROBE_SOURCES = [os.path.join(CSRC, "gather_probe.hip")]
 
 SOURCES = [os.path.join(CSRC, "dsa3d_forward.hip"), os.path.join(CSRC, "dsa3d_backward.hip"),
            os.path.join(CSRC, "dwconv3d.hip"), os.path.join(CSRC, "dsa3d_api.cpp"),
@@ -32,8 +35,14 @@ FLAGS = [
 
 
 def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, *SOURCES, "-o", tmp]
+    _compile(SOURCES, LIB, verbose)
+    _compile(PROBE_SOURCES, PROBE_LIB, verbose)
+    return LIB
+
+
+def _compile(sources, lib, verbose):
+    tmp = lib + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, *sources, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -44,8 +53,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode})")
     if verbose and errs:
         sys.stderr.write("\n".join(errs) + "\n")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
 
 
 if __name__ == "__main__":

@@ -117,6 +117,16 @@ SMALL_CASES = [
     small("grid_1x1x1", T=1, H=1, W=1, heads=2, head_dim=32, seed=21),
     small("t1_bf16", T=1, H=9, W=17, heads=2, head_dim=64, dtype="bf16", seed=22),
     small("w1_f32", T=6, H=7, W=1, heads=2, head_dim=32, seed=23),
+    # bf16 at head_dim 64 / 128 with up to 160 points runs the two-pass matrix-core forward;
+    # these cover its degenerate and mixed-size kernels and the fallback beyond 160 points
+    small("k111_bf16_d128", T=3, H=4, W=5, heads=2, head_dim=128, kt=1, kh=1, kw=1,
+          dtype="bf16", seed=26),
+    small("k135_bf16_d64", T=2, H=6, W=7, heads=3, head_dim=64, kt=1, kh=3, kw=5, dtype="bf16",
+          seed=27),
+    small("k377_bf16_d128", T=3, H=7, W=6, heads=2, head_dim=128, kt=3, kh=7, kw=7,
+          dtype="bf16", seed=28, offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
+    small("k579_bf16_d64", T=5, H=7, W=9, heads=2, head_dim=64, kt=5, kh=7, kw=9, dtype="bf16",
+          seed=29),
     # 32 heads x 512-byte fp32 rows: a token's rows exceed the buffer record stride limit, so
     # every corner takes the global-load path
     small("wide_token_f32", T=2, H=4, W=5, heads=32, head_dim=128, seed=25,
@@ -167,10 +177,12 @@ def test_single_point_integer_offsets_copy_rows_bitwise():
                                want[tuple(bad[0])])
 
 
-def test_non_finite_and_huge_offsets_are_safe():
+@pytest.mark.parametrize("dtype,dim", [("f32", 32), ("bf16", 64), ("bf16", 128)])
+def test_non_finite_and_huge_offsets_are_safe(dtype, dim):
     """Offsets of +-1e30, +-inf and NaN put every corner outside the grid: no fault, and the
     result is the all-outside one (logit 0 everywhere: out = 0, lse = ln P)."""
-    w = small("huge_offsets", T=3, H=4, W=5, heads=2, head_dim=32, seed=32)
+    w = small(f"huge_offsets_{dtype}_{dim}", T=3, H=4, W=5, heads=2, head_dim=dim, dtype=dtype,
+              seed=32)
     q, k, v, off, _ = testgen.gen_inputs(w)
     vals = np.array([1e30, -1e30, np.inf, -np.inf, np.nan], dtype=np.float32)
     off = vals[np.arange(off.size) % len(vals)].reshape(off.shape)
