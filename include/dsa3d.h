@@ -94,8 +94,8 @@ typedef struct {
 dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
                            const float* offsets, void* out, float* lse, void* stream);
 
-/* Bytes of device workspace dsa3d_backward needs for `desc`: about 60 bytes per
- * (query row, point) pair plus 8 bytes per trilinear cell.  Returns 0 for a descriptor that
+/* Bytes of device workspace dsa3d_backward needs for `desc`: about 56 bytes per
+ * (query row, point) pair plus 12 bytes per trilinear cell.  Returns 0 for a descriptor that
  * dsa3d_backward would reject. */
 size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc);
 

@@ -34,8 +34,8 @@ extern "C" {
 dsa3d_status dsa3d_pw_forward(const dsa3d_desc* desc, const float* logits, const void* v,
                               const float* offsets, void* out, float* lse, void* stream);
 
-/* Workspace bytes dsa3d_pw_backward needs (the same binning as dsa3d_backward: about 60 bytes
- * per (row, point) and 8 per cell); 0 for a descriptor it would reject. */
+/* Workspace bytes dsa3d_pw_backward needs (the same binning as dsa3d_backward: about 56 bytes
+ * per (row, point) and 12 per cell); 0 for a descriptor it would reject. */
 size_t dsa3d_pw_backward_workspace_size(const dsa3d_desc* desc);
 
 /* Backward for upstream gradient dout, with alpha_p recomputed from the logits and lse:
