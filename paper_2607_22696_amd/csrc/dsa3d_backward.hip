@@ -15,13 +15,11 @@
 //       A_p = sum_c dw_c/dpos <q, K_c>,  B_p = sum_c dw_c/dpos <dout, V_c>,
 //     so dq is final at the end of the sweep; (alpha_p, da_p, A_p, B_p) go to a 32-byte
 //     record per point.  Every point is also counted into the bin of its trilinear cell
-//     (the floor of its position) with an integer atomic whose returned value, the point's
-//     rank among the points of that bin, is stored beside the record; it is first needed at
-//     the end of the chunk, so its latency hides behind the chunk's work.
-//  2. exclusive scan of the bin counts -> bin starts.
+//     (the floor of its position) with an integer atomic whose result is not waited on.
+//  2. exclusive scan of the bin counts -> bin starts (and a copy used as fill cursors).
 //  3. finalize (one thread per point): d_offsets from A_p, B_p and the row's Delta; the
-//     point writes its dK/dV coefficients (scale ds_p, alpha_p) and fractional position to
-//     slot start(bin) + rank, i.e. sorted by cell, with plain loads and stores only.
+//     point claims a slot of its bin from the cursor and writes its dK/dV coefficients
+//     (scale ds_p, alpha_p) and fractional position there, i.e. sorted by cell.
 //  4. gather (one L-lane group per 2 x 2 block of voxels in a frame): a voxel is corner c
 //     of exactly the points whose cell is voxel - c; for the block these bins form 6
 //     contiguous runs (cells x0-1, x0, x0+1 are adjacent), and the group accumulates
@@ -88,7 +86,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
     const float* __restrict__ logits, const float* __restrict__ offsets,
     const float* __restrict__ lse, const void* __restrict__ dout, float* __restrict__ dq,
     PointRec* __restrict__ recs, float* __restrict__ delta_out, uint32_t* __restrict__ counts,
-    uint32_t* __restrict__ ranks, int tiles) {
+    int tiles) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -138,10 +136,9 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
       float mylog2 = 0.0f;  // PW: this lane's point's logit, base 2
       if constexpr (PW) mylog2 = logits[row * g.P + pm] * kLog2e;
       const bool own = p0 + sub < g.P;
-      uint32_t rank = 0;  // waited on only where the chunk's records are stored
-      if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))
-        rank = __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
-                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))  // result unused: no wait
+        __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       pm = min(p0 + L + sub, g.P - 1);  // next chunk's offsets, in flight during this one
       ox = off[3 * pm];
       oy = off[3 * pm + 1];
@@ -233,7 +230,6 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
         float4* dst = reinterpret_cast<float4*>(recs + row * g.P + p0 + sub);
         dst[0] = rec0;
         dst[1] = rec1;
-        ranks[row * g.P + p0 + sub] = rank;
       }
     }
     if constexpr (!PW) {
@@ -314,10 +310,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_sums_kernel(uint32_t* __res
   if (threadIdx.x == 0) *grand = carry;
 }
 
-// starts[x] = offset of block + exclusive scan inside the block.
+// starts[x] = cursor[x] = offset of block + exclusive scan inside the block.
 __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t* __restrict__ in,
                                                                    const uint32_t* __restrict__ sums,
                                                                    uint32_t* __restrict__ out,
+                                                                   uint32_t* __restrict__ cursor,
                                                                    int64_t n) {
   __shared__ uint32_t lds[kScanThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * kScanBlockItems + (int64_t)threadIdx.x * kScanItems;
@@ -333,7 +330,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t
   uint32_t run = sums[blockIdx.x] + excl;
 #pragma unroll
   for (int e = 0; e < kScanItems; ++e) {
-    if (base + e < n) out[base + e] = run;
+    if (base + e < n) {
+      out[base + e] = run;
+      cursor[base + e] = run;
+    }
     run += vals[e];
   }
 }
@@ -343,8 +343,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t
 // dlogits (the predicted-weights variant, else null) receives alpha_p (da_p - Delta).
 __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
     Geometry g, const float* __restrict__ offsets, const PointRec* __restrict__ recs,
-    const float* __restrict__ delta, const uint32_t* __restrict__ starts,
-    const uint32_t* __restrict__ ranks, float* __restrict__ doff,
+    const float* __restrict__ delta, uint32_t* __restrict__ cursor, float* __restrict__ doff,
     float* __restrict__ dlogits, Entry* __restrict__ entries, int npoints) {
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const unsigned P = g.P, heads = g.heads, N = g.N, W = g.W, HW = g.H * g.W;
@@ -376,7 +375,7 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
     axis((float)((int)i + (int)ih - rh), o[1], g.H, y, fy);
     axis((float)((int)t + (int)it - rt), o[2], g.T, z, fz);
     if (!cell_inside(g, x, y, z)) continue;
-    const uint32_t slot = starts[cell_index(g, b * heads + m, x, y, z)] + ranks[idx];
+    const uint32_t slot = atomicAdd(cursor + cell_index(g, b * heads + m, x, y, z), 1u);
     Entry e;
     e.n = (int32_t)n;
     e.alpha = r.alpha;
@@ -548,7 +547,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_
 struct Workspace {
   uint32_t* counts;   // [cells]
   uint32_t* starts;   // [cells + 1]
-  uint32_t* ranks;    // [rows * P]: a point's rank in its bin
+  uint32_t* cursor;   // [cells]
   uint32_t* sums;     // [ceil(cells / kScanBlockItems)]
   PointRec* recs;     // [rows * P], 16-byte aligned
   float* delta;       // [rows]
@@ -573,7 +572,7 @@ Workspace carve(const Geometry& g, void* base) {
   };
   w.counts = reinterpret_cast<uint32_t*>(take(cells * 4));
   w.starts = reinterpret_cast<uint32_t*>(take((cells + 1) * 4));
-  w.ranks = reinterpret_cast<uint32_t*>(take(points * 4));
+  w.cursor = reinterpret_cast<uint32_t*>(take(cells * 4));
   w.sums = reinterpret_cast<uint32_t*>(take(nsums * 4));
   w.recs = reinterpret_cast<PointRec*>(take(points * sizeof(PointRec)));
   w.delta = reinterpret_cast<float*>(take(rows * 4));
@@ -616,7 +615,7 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,       (void*)&v,
                  (void*)&logits, (void*)&off,  (void*)&lse,     (void*)&dout,
                  (void*)&dq,   (void*)&w.recs, (void*)&w.delta, (void*)&w.counts,
-                 (void*)&w.ranks, (void*)&tiles};
+                 (void*)&tiles};
     const void* kern = pw ? reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, true>)
                           : reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, false>);
     e = hipLaunchKernel(kern, dim3(blocks), dim3(kBlockThreads), a, 0, s);
@@ -633,7 +632,8 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_sums_kernel), dim3(1),
                         dim3(kScanThreads), b2, 0, s);
     if (e != hipSuccess) return e;
-    void* c3[] = {(void*)&w.counts, (void*)&w.sums, (void*)&w.starts, (void*)&cells};
+    void* c3[] = {(void*)&w.counts, (void*)&w.sums, (void*)&w.starts, (void*)&w.cursor,
+                  (void*)&cells};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&scan_apply_kernel), dim3((unsigned)nsums),
                         dim3(kScanThreads), c3, 0, s);
     if (e != hipSuccess) return e;
@@ -641,9 +641,9 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   if ((e = mark(2)) != hipSuccess) return e;
   {
     const int npoints = (int)points;
-    void* a[] = {(void*)&g,        (void*)&off,     (void*)&w.recs,    (void*)&w.delta,
-                 (void*)&w.starts, (void*)&w.ranks, (void*)&doff,     (void*)&dlogits,
-                 (void*)&w.entries, (void*)&npoints};
+    void* a[] = {(void*)&g,      (void*)&off,     (void*)&w.recs,    (void*)&w.delta,
+                 (void*)&w.cursor, (void*)&doff, (void*)&dlogits, (void*)&w.entries,
+                 (void*)&npoints};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_finalize_kernel), dim3(grid_for(points)),
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
