@@ -94,7 +94,8 @@ def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
            "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
            "kernels": {}}
     for k in fetch:
-        if k not in write or k == "__amd_rocclr_copyBuffer":
+        # the operator's kernels only (not the copy, fills or the gather microbenchmark)
+        if k not in write or not k.endswith("_kernel"):
             continue
         f = sum(fetch[k]) / len(fetch[k]) / fetch_scale
         w = sum(write[k]) / len(write[k]) / write_scale
