@@ -153,10 +153,6 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
         const float tx = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.ax[1])));
         const float ty = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.ay[1])));
         const float tz = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.az[1])));
-        pt.cx = __builtin_amdgcn_ds_bpermute(src, mine.cx);
-        pt.cy = __builtin_amdgcn_ds_bpermute(src, mine.cy);
-        pt.cz = __builtin_amdgcn_ds_bpermute(src, mine.cz);
-        pt.slow = __builtin_amdgcn_ds_bpermute(src, (int)mine.slow) != 0;
         pt.ax[0] = 1.0f - tx;
         pt.ax[1] = tx;
         pt.ay[0] = 1.0f - ty;
@@ -170,10 +166,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
           for (int c = 0; c < 8; ++c) pt.w[c] = pt.ax[c & 1] * wyz[c >> 1];
         }
         uint4 kr[8], vr[8];
-        if constexpr (PW)
-          load_rows<LY::kRowBytes>(g, win, win.v, vb, b, m, lane_off, pt, vr);
-        else
-          load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
+        load_shared_corners<LY::kRowBytes, !PW>(g, win, kb, vb, b, m, lane_off, mine, src,
+                                                pt.vidx, kr, vr);
         float sp = 0.0f, dap = 0.0f;
         float a3[3] = {0.0f, 0.0f, 0.0f}, b3[3] = {0.0f, 0.0f, 0.0f};
         float kp[VEC];

@@ -246,41 +246,41 @@ __device__ inline __attribute__((always_inline)) void make_point(const Geometry&
   }
 }
 
-// Loads one tensor's rows (this lane's NC x 16 bytes) at the 8 corners of a point through
-// the window resource `r`, with global loads from `base` for in-grid corners outside the
-// window; dst[c * NC + h] is chunk h of corner c.
-template <int ROW_BYTES, int NC = 1>
-__device__ inline __attribute__((always_inline)) void load_rows(
-    const Geometry& g, const RowWindow& win, __amdgpu_buffer_rsrc_t r, const char* base, int b,
-    int m, int lane_off, const Point& pt, uint4* dst) {
+// K and V rows (this lane's 16 bytes of each) at the 8 corners of a point that a lane of the
+// row formed: `vidx` are its corner indices, already fetched from that owner lane (ds_bpermute
+// address `src`, its point `mine`).  Corners come through the window resources; an in-grid
+// corner outside the window takes a global load, and the window test and the cell that load
+// needs are fetched from the owner only when some lane of the wave has such a corner (the test
+// is wave-uniform and rare), so the common case exchanges the 8 indices and one flag per
+// point.  KV = false: V only.
+template <int ROW_BYTES, bool KV>
+__device__ inline __attribute__((always_inline)) void load_shared_corners(
+    const Geometry& g, const RowWindow& win, const char* kb, const char* vb, int b, int m,
+    int lane_off, const Point& mine, int src, const int* vidx, uint4* kr, uint4* vr) {
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
-#pragma unroll
-    for (int h = 0; h < NC; ++h) dst[c * NC + h] = buffer_row(r, pt.vidx[c], lane_off + 16 * h);
+    if constexpr (KV) kr[c] = buffer_row(win.k, vidx[c], lane_off);
+    vr[c] = buffer_row(win.v, vidx[c], lane_off);
   }
-  if (pt.slow) {
+  const bool slow = __builtin_amdgcn_ds_bpermute(src, (int)mine.slow) != 0;
+  if (__builtin_amdgcn_ballot_w64(slow)) {
+    const int cx = __builtin_amdgcn_ds_bpermute(src, mine.cx);
+    const int cy = __builtin_amdgcn_ds_bpermute(src, mine.cy);
+    const int cz = __builtin_amdgcn_ds_bpermute(src, mine.cz);
+    if (slow) {
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int x = pt.cx + (c & 1), y = pt.cy + ((c >> 1) & 1), z = pt.cz + (c >> 2);
-      const bool inside = (unsigned)x < (unsigned)g.W && (unsigned)y < (unsigned)g.H &&
-                          (unsigned)z < (unsigned)g.T;
-      if (inside && (unsigned)(z - win.t0) >= (unsigned)win.frames) {
-        const int64_t row = ((((int64_t)b * g.T + z) * g.H + y) * g.W + x) * g.heads + m;
-#pragma unroll
-        for (int h = 0; h < NC; ++h)
-          dst[c * NC + h] = load16(base, row * ROW_BYTES + lane_off + 16 * h);
+      for (int c = 0; c < 8; ++c) {
+        const int x = cx + (c & 1), y = cy + ((c >> 1) & 1), z = cz + (c >> 2);
+        const bool inside = (unsigned)x < (unsigned)g.W && (unsigned)y < (unsigned)g.H &&
+                            (unsigned)z < (unsigned)g.T;
+        if (inside && (unsigned)(z - win.t0) >= (unsigned)win.frames) {
+          const int64_t row = ((((int64_t)b * g.T + z) * g.H + y) * g.W + x) * g.heads + m;
+          if constexpr (KV) kr[c] = load16(kb, row * ROW_BYTES + lane_off);
+          vr[c] = load16(vb, row * ROW_BYTES + lane_off);
+        }
       }
     }
   }
-}
-
-// K and V rows of the 8 corners of a point.
-template <int ROW_BYTES, int NC = 1>
-__device__ inline __attribute__((always_inline)) void load_corners(
-    const Geometry& g, const RowWindow& win, const char* kb, const char* vb, int b, int m,
-    int lane_off, const Point& pt, uint4* kr, uint4* vr) {
-  load_rows<ROW_BYTES, NC>(g, win, win.k, kb, b, m, lane_off, pt, kr);
-  load_rows<ROW_BYTES, NC>(g, win, win.v, vb, b, m, lane_off, pt, vr);
 }
 
 // ---------------------------------------------------------------------------- launch shape

@@ -83,18 +83,16 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
           pt.vidx[c] = __builtin_amdgcn_ds_bpermute(src, mine.vidx[c]);
           pt.w[c] = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.w[c])));
         }
-        pt.cx = __builtin_amdgcn_ds_bpermute(src, mine.cx);
-        pt.cy = __builtin_amdgcn_ds_bpermute(src, mine.cy);
-        pt.cz = __builtin_amdgcn_ds_bpermute(src, mine.cz);
-        pt.slow = __builtin_amdgcn_ds_bpermute(src, (int)mine.slow) != 0;
         uint4 vr[8];
         float s2;
         if constexpr (PW) {
-          load_rows<LY::kRowBytes>(g, win, win.v, vb, b, m, lane_off, pt, vr);
+          load_shared_corners<LY::kRowBytes, false>(g, win, kb, vb, b, m, lane_off, mine, src,
+                                                    pt.vidx, nullptr, vr);
           s2 = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mylog2)));
         } else {
           uint4 kr[8];
-          load_corners<LY::kRowBytes>(g, win, kb, vb, b, m, lane_off, pt, kr, vr);
+          load_shared_corners<LY::kRowBytes, true>(g, win, kb, vb, b, m, lane_off, mine, src,
+                                                   pt.vidx, kr, vr);
           float sp = 0.0f;
 #pragma unroll
           for (int c = 0; c < 8; ++c) sp = fmaf(pt.w[c], chunk_dot<BF16>(qr, kr[c]), sp);
