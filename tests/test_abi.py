@@ -439,3 +439,12 @@ def test_win_workspace_size_and_errors():
     need = dsa.dsa3d_win_backward_workspace_size(d)
     assert win_bwd(d, workspace=None) == B.DSA3D_ERR_WORKSPACE
     assert win_bwd(d, workspace_bytes=need - 1) == B.DSA3D_ERR_WORKSPACE
+
+
+def test_gather_probe_library_exports_its_entry_point():
+    """The gather microbenchmark bench.py reports its ceiling from is built beside the
+    library and exports its one C entry point (running it needs a GPU)."""
+    import os
+    lib = os.path.join(os.path.dirname(dsa.__file__), "libdsa3d_probe.so")
+    assert os.path.exists(lib), lib
+    assert hasattr(ctypes.CDLL(lib), "dsa3d_probe_gather")
