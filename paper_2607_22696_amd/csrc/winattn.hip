@@ -528,12 +528,17 @@ win_dq_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __r
   for (int db = 0; db < DB; ++db) store_f32_block(dq + qrow * D, db, acc[db], g.scale);
 }
 
+constexpr int kBoth = 0, kDvOnly = 1, kDkOnly = 2;
+
 // dk/dv pass: 128 keys of one group (wave w owns keys 32 w .. 32 w + 31, lanes l and l ^ 32
 // share key l % 32) against every query of the box, 64 queries per LDS tile:
 //   S = Q K^T,  P = exp2(s log2(e) scale - lse log2(e)),  dP = dout V^T,  dS = P (dP - Delta),
 //   dv^T += dout^T P,  dk^T += Q^T dS  (scaled by `scale` at the end).
-template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 2))) void
+// OUT selects the outputs: kBoth, or kDvOnly / kDkOnly, run as two launches whose accumulators
+// (half of the 128 keys' dK and dV) fit two waves per SIMD instead of one; the dV launch does
+// not form dP and the dK launch does not take P into a product.
+template <int D, int OUT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT == kBoth ? 1 : 2, 2))) void
 win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, const float* __restrict__ lse,
                 const uint16_t* __restrict__ dout, const float* __restrict__ delta,
@@ -557,9 +562,10 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
   const int uk = k0 + wave * 32 + (lane & 31);
   const bool kok = uk < n;
   const int64_t krow = kok ? row_of(g, gr.b, box_token(g, gr.bx, uk), gr.m) : 0;
+  constexpr bool kDk = OUT != kDvOnly, kDv = OUT != kDkOnly, kLean = OUT == kDkOnly && D > 64;
   bf16x8_t kf[KS], vf[KS];  // K^T and V^T as B operands
   load_frag<D>(kf, k, krow, kok);
-  load_frag<D>(vf, v, krow, kok);
+  if constexpr (kDk) load_frag<D>(vf, v, krow, kok);
 
   f32x16_t dka[DB], dva[DB];
 #pragma unroll
@@ -590,16 +596,40 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
   __syncthreads();
   fetch(tab[0], n);
   stage(0);
-  if (ntiles > 1) fetch(tab[1], n - kTile);
+  if (!kLean && ntiles > 1) fetch(tab[1], n - kTile);
   __syncthreads();
   for (int qt = 0; qt < ntiles; ++qt) {
     const uint16_t *Qc = Qs[qt & 1], *Gc = Gs[qt & 1];
     const float *Lc = Ls[qt & 1], *Dc = Dl[qt & 1];
-    if (qt + 1 < ntiles) stage((qt + 1) & 1);
-    if (qt + 2 < ntiles) fetch(tab[(qt + 2) % 3], n - (qt + 2) * kTile);
+    if constexpr (kLean) {  // no tile held in registers: the next one is loaded and stored here
+      if (qt + 1 < ntiles) {
+        fetch(tab[(qt + 1) % 3], n - (qt + 1) * kTile);
+        stage((qt + 1) & 1);
+      }
+    } else {
+      if (qt + 1 < ntiles) stage((qt + 1) & 1);
+      if (qt + 2 < ntiles) fetch(tab[(qt + 2) % 3], n - (qt + 2) * kTile);
+    }
     if (qt + 3 < ntiles) fill_rows<kTile>(tab[qt % 3], g, gr, (qt + 3) * kTile);
-    // S and dP of 32-query block qb: operands read together, then the products
+    // S and dP of 32-query block qb: operands read together, then the products; the lean form
+    // (dK alone at D = 128, to fit two waves per SIMD) reads and multiplies one operand at a time
     auto sdp = [&](int qb, f32x16_t& sa, f32x16_t& pa) {
+      if constexpr (kLean) {
+        bf16x8_t a[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) a[ks] = Tl::a_rows(Qc, qb * 32, ks);
+        __builtin_amdgcn_sched_barrier(0);
+        sa = f32x16_t{};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) sa = mfma(a[ks], kf[ks], sa);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) a[ks] = Tl::a_rows(Gc, qb * 32, ks);
+        __builtin_amdgcn_sched_barrier(0);
+        pa = f32x16_t{};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) pa = mfma(a[ks], vf[ks], pa);
+        return;
+      }
       bf16x8_t aq[KS], ag[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -612,16 +642,17 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         sa = mfma(aq[ks], kf[ks], sa);
-        pa = mfma(ag[ks], vf[ks], pa);
+        if constexpr (kDk) pa = mfma(ag[ks], vf[ks], pa);
       }
     };
     f32x16_t sc, pc;
-    sdp(0, sc, pc);
+    if constexpr (!kLean) sdp(0, sc, pc);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       // the next block's products go to the matrix cores before this block's softmax
       f32x16_t sn, pn;
-      if (qb == 0) sdp(1, sn, pn);
+      if constexpr (kLean) sdp(qb, sc, pc);
+      else if (qb == 0) sdp(1, sn, pn);
       float p[16], ds[16];
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) {  // the queries' lse and Delta
@@ -636,29 +667,35 @@ win_dkdv_kernel(WinGeometry g, const uint16_t* __restrict__ q, const uint16_t* _
         }
       }
       bf16x8_t ph[2], pl[2], dh[2], dlo[2];
-      to_frags(p, ph, pl);
-      to_frags(ds, dh, dlo);
+      if constexpr (kDv) to_frags(p, ph, pl);
+      if constexpr (kDk) to_frags(ds, dh, dlo);
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp) {
-          const bf16x8_t ag = Tl::a_cols(Gc, db * 32, qb, pp);
-          const bf16x8_t aq = Tl::a_cols(Qc, db * 32, qb, pp);
-          dva[db] = mfma(ag, ph[pp], dva[db]);
-          dva[db] = mfma(ag, pl[pp], dva[db]);
-          dka[db] = mfma(aq, dh[pp], dka[db]);
-          dka[db] = mfma(aq, dlo[pp], dka[db]);
+          if constexpr (kDv) {
+            const bf16x8_t ag = Tl::a_cols(Gc, db * 32, qb, pp);
+            dva[db] = mfma(ag, ph[pp], dva[db]);
+            dva[db] = mfma(ag, pl[pp], dva[db]);
+          }
+          if constexpr (kDk) {
+            const bf16x8_t aq = Tl::a_cols(Qc, db * 32, qb, pp);
+            dka[db] = mfma(aq, dh[pp], dka[db]);
+            dka[db] = mfma(aq, dlo[pp], dka[db]);
+          }
         }
-      sc = sn;
-      pc = pn;
+      if constexpr (!kLean) {
+        sc = sn;
+        pc = pn;
+      }
     }
     __syncthreads();
   }
   if (!kok) return;
 #pragma unroll
   for (int db = 0; db < DB; ++db) {
-    store_f32_block(dk + krow * D, db, dka[db], g.scale);
-    store_f32_block(dv + krow * D, db, dva[db], 1.0f);
+    if constexpr (kDk) store_f32_block(dk + krow * D, db, dka[db], g.scale);
+    if constexpr (kDv) store_f32_block(dv + krow * D, db, dva[db], 1.0f);
   }
 }
 
@@ -685,7 +722,11 @@ hipError_t win_backward_d(const WinGeometry& g, const uint16_t* q, const uint16_
   const float* cdelta = delta;
   void* a2[] = {(void*)&g,   (void*)&q,    (void*)&k,      (void*)&v, (void*)&lse,
                 (void*)&dout, (void*)&cdelta, (void*)&dk, (void*)&dv};
-  e = hipLaunchKernel(reinterpret_cast<const void*>(&win_dkdv_kernel<D>), grid, block, a2, 0, s);
+  e = hipLaunchKernel(reinterpret_cast<const void*>(&win_dkdv_kernel<D, kDvOnly>), grid, block,
+                      a2, 0, s);
+  if (e == hipSuccess)
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&win_dkdv_kernel<D, kDkOnly>), grid, block,
+                        a2, 0, s);
   return e == hipSuccess ? mark(events, 2, s) : e;
 }
 
