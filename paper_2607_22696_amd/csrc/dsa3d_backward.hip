@@ -542,18 +542,19 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_
 // bin entries e (points with query token n_e, coefficients sds_e and alpha_e, fractions f_e),
 //   dK[voxel] += sum_e W[voxel][e] sds_e q[n_e],   dV[voxel] += sum_e W[voxel][e] alpha_e dout[n_e],
 // W being the trilinear weight of the voxel as a corner of the entry's cell (zero when it is
-// not one of its corners).  A wave owns the 2 x 2 x 2 voxel block (x0..x0+1, y0..y0+1,
-// z0..z0+1), whose points lie in the 3 x 3 x 3 cells (x0-1..x0+1, y0-1..y0+1, z0-1..z0+1):
-// nine runs of three adjacent bins.  Per batch of 32 entries of one run
-//  * the lanes that own an entry (lane e for its dK coefficients, lane e + 32 for dV) form
-//    its 8 weighted coefficients as bf16 hi + lo pairs (about 16 significant bits) and store
-//    them as row e of A^T (voxel v = vx + 2 vy + 4 vz: hi at column 2v, lo at 2v + 1);
+// not one of its corners).  A wave owns the 4 x 2 x 2 voxel block (x0..x0+3, y0..y0+1,
+// z0..z0+1), whose points lie in the 5 x 3 x 3 cells (x0-1..x0+3, y0-1..y0+1, z0-1..z0+1):
+// nine runs of five adjacent bins.  Per batch of 32 entries of one run
+//  * the lanes that own an entry (lane e for its dK coefficient, lane e + 32 for dV) form its
+//    16 weighted coefficients (voxel v = vx + 4 vy + 8 vz) and store them as row e of A_hi^T
+//    (the upper half of each fp32 value) and of A_lo^T (the remainder rounded to bf16):
+//    hi + lo carries about 16 significant bits;
 //  * the wave copies the entries' q and dout rows into LDS;
-//  * v_mfma_f32_16x16x32_bf16 multiplies A (16 rows, 32 entries) by the rows (32 entries x 16
-//    channels per product), both operands read with the transposing ds_read_b64_tr_b16; the
-//    result rows 2v and 2v + 1 are added at the end.
+//  * v_mfma_f32_16x16x32_bf16 multiplies A_hi and A_lo (16 voxels x 32 entries) into the same
+//    accumulators by the rows (32 entries x 16 channels per product), both operands read with
+//    the transposing ds_read_b64_tr_b16.
 // Entries are loaded two batches ahead of the products and rows one batch ahead.  Each wave
-// has its own LDS and LDS operations of a wave complete in order, so there are no barriers.
+// has its own LDS and the LDS operations of a wave complete in order, so there are no barriers.
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -562,20 +563,23 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int kGB = 32;  // entries per batch: the products' K
 
+// waves per workgroup: the LDS of a wave grows with head_dim
+template <int D>
+constexpr int gather_waves() { return D <= 64 ? 4 : 2; }
+
 template <int D, bool PW>
 struct GatherLds {
   uint16_t q[PW ? 8 : kGB * D];  // the batch's rows, 16-byte chunks permuted per row
   uint16_t g[kGB * D];
-  uint16_t ak[PW ? 8 : kGB * 16];  // A^T of the dK products: 32 rows of 16 bf16
-  uint16_t av[kGB * 16];
-  uint4 run[9];  // (first entry, cell x0 start, cell x0 + 1 start, end) of the non-empty runs
-  int rc[9];     // their cell row / plane: (y - y0 + 1) + 3 (z - z0 + 1)
+  uint16_t a[PW ? 2 : 4][kGB * 16];  // A^T: (dV hi, dV lo[, dK hi, dK lo]), 32 rows of 16 bf16
+  uint4 run[9][2];  // cell starts x0-1 .. x0+3 and the end, of the non-empty runs
+  int rc[9];        // their cell row / plane: (y - y0 + 1) + 3 (z - z0 + 1)
 };
 
-// The 16-byte chunks of row e are permuted by XOR with 2 s(e), so that each 16-lane group of a
-// transposing read (4 rows x 32 bytes, rows 8 G + {0..3} or 8 G + {4..7} for group G) and each
-// half-wave of it (groups 0, 1 or 2, 3) reads 256 distinct bytes of banks; the row-wise 16-byte
-// writes stay conflict-free since a row keeps its bytes.
+// The 16-byte chunks of row e are permuted by XOR with 2 s(e), so that each half-wave of a
+// transposing read (for groups G = 0, 1 or 2, 3: rows 8 G + {0..3}, or 8 G + {4..7}, 32 bytes
+// each) covers 256 distinct bytes of banks; the row-wise 16-byte writes stay conflict-free since
+// a row keeps its bytes.
 template <int D>
 __device__ inline int gather_row_at(int e, int chunk) {
   int s;
@@ -611,7 +615,7 @@ __device__ inline bf16x8_t gather_a_frag(const uint16_t* at) {
   return tr_pair(base + gather_at_at(e) + in, base + gather_at_at(e + 4) + in);
 }
 
-// Weights of voxel coordinate 0 and 1 of the block along one axis for a cell at offset rc
+// Weights of voxel coordinates 0 and 1 of the block along y or z for a cell at offset rc
 // (-1, 0, 1) from the block: the cell's lower corner takes 1 - f, its upper corner f.
 __device__ inline void axis_weights(float f, int rc, float& w0, float& w1) {
   const float lo = 1.0f - f;
@@ -619,97 +623,108 @@ __device__ inline void axis_weights(float f, int rc, float& w0, float& w1) {
   w1 = rc < 0 ? 0.0f : (rc == 0 ? f : lo);
 }
 
-// Row of A^T for one entry: c times the weights of the block's 8 voxels, each as bf16 hi (the
-// upper half of the fp32 value) and lo (the remainder, rounded to nearest even).
-__device__ inline void weight_row(float c, float fx, float fy, float fz, int rcx, int rcy,
-                                  int rcz, uint32_t (&d)[8]) {
-  float x[2], y[2], z[2];
-  axis_weights(fx, rcx, x[0], x[1]);
+// Rows of A_hi^T and A_lo^T for one entry: c times the weights of the block's 16 voxels.
+__device__ inline void weight_rows(float c, float fx, float fy, float fz, int rcx, int rcy,
+                                   int rcz, uint32_t (&hi)[8], uint32_t (&lo)[8]) {
+  float x[4], y[2], z[2];
+  const float fl = 1.0f - fx;
+#pragma unroll
+  for (int vx = 0; vx < 4; ++vx) x[vx] = vx == rcx ? fl : (vx == rcx + 1 ? fx : 0.0f);
   axis_weights(fy, rcy, y[0], y[1]);
   axis_weights(fz, rcz, z[0], z[1]);
-  float w[8];
+  float w[16];
 #pragma unroll
-  for (int v = 0; v < 8; ++v) w[v] = x[v & 1] * (y[(v >> 1) & 1] * (c * z[v >> 2]));
+  for (int v = 0; v < 16; ++v) w[v] = x[v & 3] * (y[(v >> 2) & 1] * (c * z[v >> 3]));
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
+  for (int p = 0; p < 8; ++p) {
     const uint32_t u0 = __float_as_uint(w[2 * p]), u1 = __float_as_uint(w[2 * p + 1]);
+    hi[p] = __builtin_amdgcn_perm(u1, u0, 0x07060302u);  // upper halves of w0 (low), w1 (high)
     const float l0 = w[2 * p] - __uint_as_float(u0 & 0xffff0000u);
     const float l1 = w[2 * p + 1] - __uint_as_float(u1 & 0xffff0000u);
-    const uint32_t lp = __builtin_bit_cast(uint32_t, bf16x2_t{(__bf16)l0, (__bf16)l1});
-    d[2 * p] = __builtin_amdgcn_perm(u0, lp, 0x01000706u);      // hi(w0) | lo(w0) << 16
-    d[2 * p + 1] = __builtin_amdgcn_perm(u1, lp, 0x03020706u);  // hi(w1) | lo(w1) << 16
+    lo[p] = __builtin_bit_cast(uint32_t, bf16x2_t{(__bf16)l0, (__bf16)l1});
   }
 }
 
-// A batch position: entries [u, min(u + 32, end)) of run r, whose cells x0 - 1, x0, x0 + 1
-// start at u0 <= m1 <= m2; u >= end once the runs are exhausted.
+// A batch position: entries [u, min(u + 32, end)) of run r, whose cells x0 - 1 + i start at
+// m[i] (m[0] <= u); u >= end once the runs are exhausted.
 struct GatherPos {
-  uint32_t u, end, m1, m2;
+  uint32_t u, end, m1, m2, m3, m4;
   int rc, r;
 };
 
+// This lane's 16 bytes of an entry: lanes 0-31 read (n, alpha, sds, fx), lanes 32-63 read
+// (sds, fx, fy, fz) of the same entry; the halves then swap what the other one holds.
+struct GatherEntry {
+  uint4 raw;
+  uint32_t idx;
+};
+
 template <int D, bool PW>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 3 : 2)))
+__global__ __launch_bounds__(64 * gather_waves<D>()) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 3 : 2)))
 void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* __restrict__ dout,
                             const uint32_t* __restrict__ starts, const Entry* __restrict__ entries,
                             float* __restrict__ dk, float* __restrict__ dv, int tiles) {
-  constexpr int DB = D / 16;     // 16-channel blocks: one product each per tensor
+  constexpr int NW = gather_waves<D>();
+  constexpr int DB = D / 16;     // 16-channel blocks: two products each (hi, lo) per tensor
   constexpr int LPR = D / 8;     // lanes per row when copying rows (16 bytes each)
   constexpr int RPI = 64 / LPR;  // rows per copy instruction
   constexpr int NI = kGB / RPI;  // copy instructions per tensor and batch
-  __shared__ GatherLds<D, PW> lds[kWavesPerBlock];
+  __shared__ GatherLds<D, PW> lds[NW];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   GatherLds<D, PW>& L = lds[wave];
-  const int Xb = (g.W + 1) / 2, Yb = (g.H + 1) / 2, Zb = (g.T + 1) / 2;
+  const int Xb = (g.W + 3) / 4, Yb = (g.H + 1) / 2, Zb = (g.T + 1) / 2;
   const int nblk = Xb * Yb * Zb;  // voxel blocks per (b, head)
-  const int tiles_per_bh = (nblk + kWavesPerBlock - 1) / kWavesPerBlock;
+  const int tiles_per_bh = (nblk + NW - 1) / NW;
   const uint32_t tok_bytes = (uint32_t)g.heads * 2 * D;
-  const int own = lane & 31;  // the entry whose coefficients this lane forms
+  const bool upper = lane >= 32;  // dV coefficients (else dK)
+  const int own = lane & 31;      // the entry whose coefficients this lane forms
 
   for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
-    const int blk = (tile % tiles_per_bh) * kWavesPerBlock + wave;
+    const int blk = (tile % tiles_per_bh) * NW + wave;
     if (blk >= nblk) continue;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int x0 = 2 * (blk % Xb), y0 = 2 * ((blk / Xb) % Yb), z0 = 2 * (blk / (Xb * Yb));
-    const bool hasx1 = x0 + 1 < g.W, hasy1 = y0 + 1 < g.H, hasz1 = z0 + 1 < g.T;
+    const int x0 = 4 * (blk % Xb), y0 = 2 * ((blk / Xb) % Yb), z0 = 2 * (blk / (Xb * Yb));
+    const int nx = min(5, g.W - x0 + 1);  // cells x0 - 1 .. x0 + nx - 2 exist
+    const bool hasy1 = y0 + 1 < g.H, hasz1 = z0 + 1 < g.T;
     const int64_t head_off = ((int64_t)b * g.N * g.heads + m) * (2 * D) + (lane % LPR) * 16;
     const char* qh = static_cast<const char*>(q) + head_off;
     const char* gh = static_cast<const char*>(dout) + head_off;
 
     // the non-empty runs, in order: lane r < 9 looks at cell row y0 - 1 + r % 3, plane z0 - 1 + r / 3
     bool has = false;
-    uint4 rt = make_uint4(0, 0, 0, 0);
+    uint32_t c[6] = {0u, 0u, 0u, 0u, 0u, 0u};
     if (lane < 9) {
       const int yr = lane % 3, zr = lane / 3;
       if ((yr < 2 || hasy1) && (zr < 2 || hasz1)) {
         const int64_t ci = cell_index(g, bh, x0 - 1, y0 - 1 + yr, z0 - 1 + zr);
-        rt.x = starts[ci];
-        rt.y = starts[ci + 1];
-        rt.z = starts[ci + 2];
-        rt.w = hasx1 ? starts[ci + 3] : rt.z;
-        has = rt.x < rt.w;
+#pragma unroll
+        for (int i = 0; i < 6; ++i) c[i] = starts[ci + min(i, nx)];
+        has = c[0] < c[5];
       }
     }
     const uint64_t hm = __builtin_amdgcn_ballot_w64(has);
     const int nruns = __popcll(hm);
     if (has) {
       const int at = __popcll(hm & ((1ull << lane) - 1ull));
-      L.run[at] = rt;
+      L.run[at][0] = make_uint4(c[0], c[1], c[2], c[3]);
+      L.run[at][1] = make_uint4(c[4], c[5], 0u, 0u);
       L.rc[at] = lane;
     }
     auto load_run = [&](GatherPos& d, int r) {
       d.r = r;
       if (r < nruns) {
-        const uint4 t = L.run[r];
-        d.u = __builtin_amdgcn_readfirstlane(t.x);
-        d.m1 = __builtin_amdgcn_readfirstlane(t.y);
-        d.m2 = __builtin_amdgcn_readfirstlane(t.z);
-        d.end = __builtin_amdgcn_readfirstlane(t.w);
+        const uint4 t0 = L.run[r][0], t1 = L.run[r][1];
+        d.u = __builtin_amdgcn_readfirstlane(t0.x);
+        d.m1 = __builtin_amdgcn_readfirstlane(t0.y);
+        d.m2 = __builtin_amdgcn_readfirstlane(t0.z);
+        d.m3 = __builtin_amdgcn_readfirstlane(t0.w);
+        d.m4 = __builtin_amdgcn_readfirstlane(t1.x);
+        d.end = __builtin_amdgcn_readfirstlane(t1.y);
         d.rc = __builtin_amdgcn_readfirstlane(L.rc[r]);
       } else {
-        d.u = d.end = d.m1 = d.m2 = 0u;
+        d.u = d.end = d.m1 = d.m2 = d.m3 = d.m4 = 0u;
         d.rc = 0;
       }
     };
@@ -717,30 +732,43 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
       d.u += kGB;
       if (d.u >= d.end) load_run(d, d.r + 1);
     };
-    // this lane's entry of a batch (clamped to the run; its coefficient is zeroed outside it)
-    auto fetch = [&](const GatherPos& d, Entry& en, uint32_t& idx) {
-      idx = d.u + own;
-      en = entries[min(idx, d.end - 1u)];
+    // this lane's part of its entry (clamped to the run; the coefficient is zeroed outside it)
+    auto fetch = [&](const GatherPos& d, GatherEntry& en) {
+      en.idx = d.u + own;
+      const char* p = reinterpret_cast<const char*>(entries + min(en.idx, d.end - 1u));
+      en.raw = *reinterpret_cast<const uint4*>(p + (upper ? 8 : 0));
     };
-    auto weights = [&](const GatherPos& d, const Entry& en, uint32_t idx) {
-      const int rcx = -1 + (idx >= d.m1 ? 1 : 0) + (idx >= d.m2 ? 1 : 0);
-      const bool dvl = lane >= 32;
-      if (PW && !dvl) return;
-      const float c = idx < d.end ? (dvl ? en.alpha : en.sds) : 0.0f;
-      uint32_t w[8];
-      weight_row(c, en.fx, en.fy, en.fz, rcx, d.rc % 3 - 1, d.rc / 3 - 1, w);
-      char* at = reinterpret_cast<char*>(dvl ? L.av : L.ak) + gather_at_at(own);
-      *reinterpret_cast<uint4*>(at) = make_uint4(w[0], w[1], w[2], w[3]);
-      *reinterpret_cast<uint4*>(at + 16) = make_uint4(w[4], w[5], w[6], w[7]);
+    auto weights = [&](const GatherPos& d, const GatherEntry& en) {
+      // the other half's words: lanes 0-31 get (fy, fz), lanes 32-63 get alpha
+      const auto sz = __builtin_amdgcn_permlane32_swap(en.raw.z, en.raw.z, false, false);
+      const auto sw = __builtin_amdgcn_permlane32_swap(en.raw.w, en.raw.w, false, false);
+      const auto sy = __builtin_amdgcn_permlane32_swap(en.raw.y, en.raw.y, false, false);
+      const float coef = __uint_as_float(upper ? sy[0] : en.raw.z);
+      const float fx = __uint_as_float(upper ? en.raw.y : en.raw.w);
+      const float fy = __uint_as_float(upper ? en.raw.z : sz[1]);
+      const float fz = __uint_as_float(upper ? en.raw.w : sw[1]);
+      const uint32_t i = en.idx;
+      const int rcx = -1 + (i >= d.m1 ? 1 : 0) + (i >= d.m2 ? 1 : 0) + (i >= d.m3 ? 1 : 0) +
+                      (i >= d.m4 ? 1 : 0);
+      if (PW && !upper) return;
+      uint32_t hi[8], lo[8];
+      weight_rows(i < d.end ? coef : 0.0f, fx, fy, fz, rcx, d.rc % 3 - 1, d.rc / 3 - 1, hi, lo);
+      const int sel = upper ? 0 : 2;
+      char* ah = reinterpret_cast<char*>(L.a[sel]) + gather_at_at(own);
+      char* al = reinterpret_cast<char*>(L.a[sel + 1]) + gather_at_at(own);
+      *reinterpret_cast<uint4*>(ah) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+      *reinterpret_cast<uint4*>(ah + 16) = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+      *reinterpret_cast<uint4*>(al) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      *reinterpret_cast<uint4*>(al + 16) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
     };
     uint4 rq[NI], rg[NI];
     uint32_t rok = 0;  // bit t: copy t's row is an entry of the batch
-    auto issue_rows = [&](const GatherPos& d, const Entry& en) {
+    auto issue_rows = [&](const GatherPos& d, const GatherEntry& en) {
       rok = 0;
 #pragma unroll
       for (int t = 0; t < NI; ++t) {
         const int e = lane / LPR + RPI * t;
-        const uint32_t n = (uint32_t)__shfl(en.n, e);
+        const uint32_t n = (uint32_t)__shfl((int)en.raw.x, e);  // lanes 0-31 hold n
         const uint64_t o = (uint64_t)n * tok_bytes;
         if constexpr (!PW) rq[t] = *reinterpret_cast<const uint4*>(qh + o);
         rg[t] = *reinterpret_cast<const uint4*>(gh + o);
@@ -765,52 +793,58 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
     GatherPos d0, d1, d2;
     load_run(d0, 0);
     if (d0.u < d0.end) {
-      Entry e0, e1, e2;
-      uint32_t i0, i1, i2;
-      fetch(d0, e0, i0);
-      weights(d0, e0, i0);
+      GatherEntry e0, e1, e2;
+      fetch(d0, e0);
+      weights(d0, e0);
       issue_rows(d0, e0);
       d1 = d0;
       advance(d1);
-      if (d1.u < d1.end) fetch(d1, e1, i1);
+      if (d1.u < d1.end) fetch(d1, e1);
       d2 = d1;
       advance(d2);
       while (d0.u < d0.end) {
         store_rows();
-        if (d2.u < d2.end) fetch(d2, e2, i2);
+        if (d2.u < d2.end) fetch(d2, e2);
         if (d1.u < d1.end) issue_rows(d1, e1);
-        const bf16x8_t av = gather_a_frag(L.av);
-        bf16x8_t ak;
-        if constexpr (!PW) ak = gather_a_frag(L.ak);
+        const bf16x8_t avh = gather_a_frag(L.a[0]), avl = gather_a_frag(L.a[1]);
+        bf16x8_t akh, akl;
+        if constexpr (!PW) {
+          akh = gather_a_frag(L.a[2]);
+          akl = gather_a_frag(L.a[3]);
+        }
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          if constexpr (!PW)
-            ck[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, gather_b_frag<D>(L.q, db), ck[db], 0, 0, 0);
-          cv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, gather_b_frag<D>(L.g, db), cv[db], 0, 0, 0);
+          if constexpr (!PW) {
+            const bf16x8_t bq = gather_b_frag<D>(L.q, db);
+            ck[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(akh, bq, ck[db], 0, 0, 0);
+            ck[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(akl, bq, ck[db], 0, 0, 0);
+          }
+          const bf16x8_t bg = gather_b_frag<D>(L.g, db);
+          cv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(avh, bg, cv[db], 0, 0, 0);
+          cv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(avl, bg, cv[db], 0, 0, 0);
         }
-        if (d1.u < d1.end) weights(d1, e1, i1);
+        if (d1.u < d1.end) weights(d1, e1);
         e1 = e2;
-        i1 = i2;
         d0 = d1;
         d1 = d2;
         advance(d2);
       }
     }
 
-    // result rows 4 G + {0, 1} are voxel 2 G (hi, lo), rows 4 G + {2, 3} voxel 2 G + 1
+    // result rows 4 G + vx (G = lane / 16 = vy + 2 vz), column lane % 16 of each channel block
     const int grp = lane >> 4, col = lane & 15;
     const int vy = grp & 1, vz = grp >> 1;
     if ((vy == 0 || hasy1) && (vz == 0 || hasz1)) {
       const int64_t row0 =
           ((int64_t)b * g.N + (int64_t)((z0 + vz) * g.H + y0 + vy) * g.W + x0) * g.heads + m;
 #pragma unroll
-      for (int vx = 0; vx < 2; ++vx) {
-        if (vx == 1 && !hasx1) break;
+      for (int vx = 0; vx < 4; ++vx) {
+        if (vx > 0 && x0 + vx >= g.W) break;
         const int64_t row = row0 + (int64_t)vx * g.heads;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          if constexpr (!PW) dk[row * D + db * 16 + col] = ck[db][2 * vx] + ck[db][2 * vx + 1];
-          dv[row * D + db * 16 + col] = cv[db][2 * vx] + cv[db][2 * vx + 1];
+          if constexpr (!PW) dk[row * D + db * 16 + col] = ck[db][vx];
+          dv[row * D + db * 16 + col] = cv[db][vx];
         }
       }
     }
@@ -925,15 +959,15 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   }
   if ((e = mark(3)) != hipSuccess) return e;
   if constexpr (BF16) {
-    const int64_t vblocks = (int64_t)((g.T + 1) / 2) * ((g.H + 1) / 2) * ((g.W + 1) / 2);
-    const int gtiles =
-        (int)((vblocks + kWavesPerBlock - 1) / kWavesPerBlock * g.B * g.heads);
+    constexpr int NW = gather_waves<D>();
+    const int64_t vblocks = (int64_t)((g.T + 1) / 2) * ((g.H + 1) / 2) * ((g.W + 3) / 4);
+    const int gtiles = (int)((vblocks + NW - 1) / NW * g.B * g.heads);
     const int gblocks = gtiles < kMaxBlocks ? gtiles : kMaxBlocks;
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
                  (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&gtiles};
     const void* kern = pw ? reinterpret_cast<const void*>(&bwd_gather_mfma_kernel<D, true>)
                           : reinterpret_cast<const void*>(&bwd_gather_mfma_kernel<D, false>);
-    e = hipLaunchKernel(kern, dim3(gblocks), dim3(kBlockThreads), a, 0, s);
+    e = hipLaunchKernel(kern, dim3(gblocks), dim3(64 * NW), a, 0, s);
     if (e != hipSuccess) return e;
   } else {
     using LY = Layout<D, BF16>;
