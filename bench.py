@@ -179,14 +179,15 @@ def vmem_bytes(w):
 def gather_ceiling(row_bytes):
     """The gather microbenchmark (libdsa3d_probe.so): 16-byte lane loads, one contiguous row
     of row_bytes per lane group at pseudo-random addresses, every row already in L1 (the
-    ceiling of the kernels' gather path), and the same pattern from LDS."""
+    ceiling of the kernels' gather path), every row missing L1 and hitting L2, and the same
+    pattern from LDS."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_22696_amd", "libdsa3d_probe.so"))
     lib.dsa3d_probe_gather.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.POINTER(ctypes.c_float),
                                        ctypes.POINTER(ctypes.c_double)]
     out = {"row_bytes": row_bytes}
-    for src, name in ((0, "l1"), (1, "lds")):
+    for src, name in ((0, "l1"), (2, "l2"), (1, "lds")):
         ms, nb = ctypes.c_float(), ctypes.c_double()
         rc = lib.dsa3d_probe_gather(src, row_bytes, 2048, 4096, ctypes.byref(ms), ctypes.byref(nb))
         if rc != 0:
@@ -195,18 +196,28 @@ def gather_ceiling(row_bytes):
     return out
 
 
-def roofline(work, ms):
-    """Roofline entry of one kernel: bound by whichever of HBM bytes and fp32 VALU flops takes
-    longer at peak; achieved = algorithmic work per launch / average launch time."""
+def roofline(work, ms, peak=VALU_PEAK_TFLOPS, bound="alu"):
+    """Roofline entry of one kernel: bound by whichever of HBM bytes and its flops takes
+    longer at peak (fp32 vector peak; the dense bf16 matrix peak for a kernel whose
+    multiply-adds run on the matrix cores); achieved = algorithmic work per launch / average
+    launch time."""
     t_hbm = work["bytes"] / (HBM_PEAK_GBS * 1e9)
-    t_alu = work["flops"] / (VALU_PEAK_TFLOPS * 1e12)
+    t_alu = work["flops"] / (peak * 1e12)
     if t_alu >= t_hbm:
         ach = work["flops"] / (ms * 1e-3) / 1e12
-        return {"bound": "alu", "achieved": round(ach, 3), "peak": VALU_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / VALU_PEAK_TFLOPS, 4)}
+        return {"bound": bound, "achieved": round(ach, 3), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(ach / peak, 4)}
     ach = work["bytes"] / (ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+
+def kernel_roofline(w, alg, name, ms):
+    """The bf16 dK/dV gather takes its multiply-adds on the matrix cores; the other kernels
+    on the vector ALUs."""
+    if name == "bwd_gather_kernel" and w.dtype == "bf16":
+        return roofline(alg[name], ms, MFMA_BF16_PEAK_TFLOPS, "mfma")
+    return roofline(alg[name], ms)
 
 
 def cpu_baseline(w, host, budget_s, backward=True):
@@ -429,7 +440,7 @@ def bench_pw(args, torch, dsa, testgen, to_device):
         kernel_ms[n] = sum(p[i].elapsed_time(p[i + 1]) for p in ph) / K
     alg = pw_algorithmic(w)
     kname = max((n for n in kernel_ms if n in alg), key=lambda n: kernel_ms[n])
-    roof = roofline(alg[kname], kernel_ms[kname])
+    roof = kernel_roofline(w, alg, kname, kernel_ms[kname])
     roof["traffic"] = None
     roof["kernel"] = kname
     roof["avg_launch_ms"] = round(kernel_ms[kname], 4)
@@ -443,7 +454,8 @@ def bench_pw(args, torch, dsa, testgen, to_device):
                    "heads": w.heads, "head_dim": w.head_dim, "kernel": [w.kt, w.kh, w.kw],
                    "points": w.P, "backward": True, "parallelism": "single GPU"},
         "kernel_ms": {n: round(t, 4) for n, t in kernel_ms.items()},
-        "kernel_roofline": {n: roofline(alg[n], t) for n, t in kernel_ms.items() if n in alg},
+        "kernel_roofline": {n: kernel_roofline(w, alg, n, t) for n, t in kernel_ms.items()
+                            if n in alg},
         "hbm_gbs_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "roofline": roof, "input_gen_s": round(t_gen, 1),
@@ -755,7 +767,7 @@ def main():
     tokens = w.B * w.N
     # dominant kernel: the longest single kernel of the step
     kname = max((n for n in kernel_ms if n in alg), key=lambda n: kernel_ms[n])
-    roof = roofline(alg[kname], kernel_ms[kname])
+    roof = kernel_roofline(w, alg, kname, kernel_ms[kname])
     tr = measured_traffic(w.name, kname)
     roof["traffic"] = None if tr is None else round(tr)
     roof["kernel"] = kname
@@ -790,7 +802,8 @@ def main():
         "fwd_ms": round(fwd_ms, 4),
         "bwd_ms": round(bwd_ms, 4),
         "kernel_ms": {n: round(t, 4) for n, t in kernel_ms.items()},
-        "kernel_roofline": {n: roofline(alg[n], t) for n, t in kernel_ms.items() if n in alg},
+        "kernel_roofline": {n: kernel_roofline(w, alg, n, t) for n, t in kernel_ms.items()
+                            if n in alg},
         "hbm_gbs_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "token_head_rows_per_s": round(w.queries / (ms_step * 1e-3), 1),

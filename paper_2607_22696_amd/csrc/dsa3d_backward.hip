@@ -762,27 +762,35 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
       *reinterpret_cast<uint4*>(al + 16) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
     };
     uint4 rq[NI], rg[NI];
-    uint32_t rok = 0;  // bit t: copy t's row is an entry of the batch
+    bool part = false;  // the batch ends inside: its rows past the end are zeroed in LDS
     auto issue_rows = [&](const GatherPos& d, const GatherEntry& en) {
-      rok = 0;
+      part = d.end - d.u < (uint32_t)kGB;
 #pragma unroll
       for (int t = 0; t < NI; ++t) {
         const int e = lane / LPR + RPI * t;
         const uint32_t n = (uint32_t)__shfl((int)en.raw.x, e);  // lanes 0-31 hold n
         const uint64_t o = (uint64_t)n * tok_bytes;
-        if constexpr (!PW) rq[t] = *reinterpret_cast<const uint4*>(qh + o);
-        rg[t] = *reinterpret_cast<const uint4*>(gh + o);
-        rok |= (d.u + e < d.end ? 1u : 0u) << t;
+        if (d.u + e < d.end) {  // rows past the run's end are not loaded
+          if constexpr (!PW) rq[t] = *reinterpret_cast<const uint4*>(qh + o);
+          rg[t] = *reinterpret_cast<const uint4*>(gh + o);
+        }
       }
     };
-    auto store_rows = [&]() {
+    auto store_rows = [&](const GatherPos& d) {
+      if (part) {
+#pragma unroll
+        for (int t = 0; t < NI; ++t) {
+          if (d.u + lane / LPR + RPI * t >= d.end) {
+            rq[t] = make_uint4(0, 0, 0, 0);
+            rg[t] = make_uint4(0, 0, 0, 0);
+          }
+        }
+      }
 #pragma unroll
       for (int t = 0; t < NI; ++t) {
-        const int e = lane / LPR + RPI * t, at = gather_row_at<D>(e, lane % LPR);
-        const bool ok = (rok >> t) & 1u;
-        if constexpr (!PW)
-          *reinterpret_cast<uint4*>(reinterpret_cast<char*>(L.q) + at) = ok ? rq[t] : make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4*>(reinterpret_cast<char*>(L.g) + at) = ok ? rg[t] : make_uint4(0, 0, 0, 0);
+        const int at = gather_row_at<D>(lane / LPR + RPI * t, lane % LPR);
+        if constexpr (!PW) *reinterpret_cast<uint4*>(reinterpret_cast<char*>(L.q) + at) = rq[t];
+        *reinterpret_cast<uint4*>(reinterpret_cast<char*>(L.g) + at) = rg[t];
       }
     };
 
@@ -790,22 +798,28 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
 #pragma unroll
     for (int db = 0; db < DB; ++db) ck[db] = cv[db] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-    GatherPos d0, d1, d2;
-    load_run(d0, 0);
-    if (d0.u < d0.end) {
-      GatherEntry e0, e1, e2;
-      fetch(d0, e0);
-      weights(d0, e0);
-      issue_rows(d0, e0);
-      d1 = d0;
-      advance(d1);
-      if (d1.u < d1.end) fetch(d1, e1);
-      d2 = d1;
-      advance(d2);
-      while (d0.u < d0.end) {
-        store_rows();
-        if (d2.u < d2.end) fetch(d2, e2);
-        if (d1.u < d1.end) issue_rows(d1, e1);
+    // Per batch i: store its rows, fetch the entries of batch i + 2, load the rows of batch
+    // i + 1, take batch i's products, then form batch i + 1's weights (p0, p1, p2: batches i,
+    // i + 1, i + 2).
+    GatherPos p0, p1, p2;
+    load_run(p0, 0);
+    if (p0.u < p0.end) {
+      GatherEntry e1, e2;
+      {
+        GatherEntry e0;
+        fetch(p0, e0);
+        weights(p0, e0);
+        issue_rows(p0, e0);
+      }
+      p1 = p0;
+      advance(p1);
+      if (p1.u < p1.end) fetch(p1, e1);
+      p2 = p1;
+      advance(p2);
+      while (p0.u < p0.end) {
+        store_rows(p0);
+        if (p2.u < p2.end) fetch(p2, e2);
+        if (p1.u < p1.end) issue_rows(p1, e1);
         const bf16x8_t avh = gather_a_frag(L.a[0]), avl = gather_a_frag(L.a[1]);
         bf16x8_t akh, akl;
         if constexpr (!PW) {
@@ -823,11 +837,11 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
           cv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(avh, bg, cv[db], 0, 0, 0);
           cv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(avl, bg, cv[db], 0, 0, 0);
         }
-        if (d1.u < d1.end) weights(d1, e1);
+        if (p1.u < p1.end) weights(p1, e1);
         e1 = e2;
-        d0 = d1;
-        d1 = d2;
-        advance(d2);
+        p0 = p1;
+        p1 = p2;
+        advance(p2);
       }
     }
 

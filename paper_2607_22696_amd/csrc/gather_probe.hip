@@ -6,11 +6,12 @@
 // pattern when every row already sits in the unit's vector L1 cache (a 16 KB working set per
 // workgroup), and, for comparison, from LDS (ds_read_b128 into a 64 KB LDS array).  The L1
 // figure is the ceiling of the operator's gather path: a kernel whose rows also miss L1 can
-// only be slower.
+// only be slower.  A third mode reads rows at random from a 2 MB region shared by all
+// workgroups: it misses L1 and hits L2, the rate of rows that the vector L1 does not hold.
 //
 // Every index is masked into its buffer: lds_gather touches slots [0, 4096) of its 64 KB
 // array, l1_gather slots [0, 1024) of its block's 16 KB region of the source buffer, whose
-// 256 regions the host allocates (4 MB).
+// 256 regions the host allocates (4 MB), l2_gather slots [0, 131072) of that buffer.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -20,6 +21,7 @@ constexpr int kThreads = 256;
 constexpr int kLdsSlots = 65536 / 16;  // 16-byte slots of the LDS array
 constexpr int kL1Slots = 16384 / 16;   // 16-byte slots of one block's L1-resident region
 constexpr int kRegions = 256;
+constexpr int kL2Slots = (2 << 20) / 16;  // 16-byte slots of the L2-resident region
 
 template <int GS>
 __global__ __launch_bounds__(kThreads) void lds_gather(uint4* out, int iters, uint32_t seed) {
@@ -62,27 +64,53 @@ __global__ __launch_bounds__(kThreads) void l1_gather(const uint4* __restrict__ 
   out[blockIdx.x * kThreads + threadIdx.x] = acc;
 }
 
+template <int GS>
+__global__ __launch_bounds__(kThreads) void l2_gather(const uint4* __restrict__ src, uint4* out,
+                                                      int iters, uint32_t seed) {
+  uint32_t h = (threadIdx.x / GS) * 2654435761u + seed + blockIdx.x * 97u;
+  const int part = threadIdx.x % GS;
+  uint4 acc = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll 8
+  for (int it = 0; it < iters; ++it) {
+    h = h * 1664525u + 1013904223u;
+    const uint32_t idx = ((h >> 4) & (kL2Slots / GS - 1)) * GS + part;
+    const uint4 v = src[idx];
+    acc.x ^= v.x;
+    acc.y += v.y;
+    acc.z ^= v.z;
+    acc.w += v.w;
+  }
+  out[blockIdx.x * kThreads + threadIdx.x] = acc;
+}
+
 }  // namespace
 
 extern "C" {
 
-// Runs the gather of `source` (0: L1-resident global loads, 1: LDS) with row pieces of
+// Runs the gather of `source` (0: L1-resident global loads, 1: LDS, 2: global loads that miss
+// L1 and hit L2) with row pieces of
 // `row_bytes` (32, 64, 128 or 256: GS = row_bytes / 16 lanes per row) over `blocks`
 // workgroups of `iters` loads per lane, twice; stores the second run's time in *ms and the
 // bytes gathered per run in *bytes.  Returns 0, or a nonzero hipError_t / -1 for arguments
 // outside those values.  Allocates and frees its own buffers and synchronises the device.
 int dsa3d_probe_gather(int source, int row_bytes, int blocks, int iters, float* ms,
                        double* bytes) {
-  if (ms == nullptr || bytes == nullptr || blocks < 1 || iters < 1 || (source != 0 && source != 1))
+  if (ms == nullptr || bytes == nullptr || blocks < 1 || iters < 1 || source < 0 || source > 2)
     return -1;
-  const void* fn = nullptr;
+  const void* fns[4][3] = {
+      {(const void*)&l1_gather<2>, (const void*)&lds_gather<2>, (const void*)&l2_gather<2>},
+      {(const void*)&l1_gather<4>, (const void*)&lds_gather<4>, (const void*)&l2_gather<4>},
+      {(const void*)&l1_gather<8>, (const void*)&lds_gather<8>, (const void*)&l2_gather<8>},
+      {(const void*)&l1_gather<16>, (const void*)&lds_gather<16>, (const void*)&l2_gather<16>}};
+  int ri;
   switch (row_bytes) {
-    case 32: fn = source ? (const void*)&lds_gather<2> : (const void*)&l1_gather<2>; break;
-    case 64: fn = source ? (const void*)&lds_gather<4> : (const void*)&l1_gather<4>; break;
-    case 128: fn = source ? (const void*)&lds_gather<8> : (const void*)&l1_gather<8>; break;
-    case 256: fn = source ? (const void*)&lds_gather<16> : (const void*)&l1_gather<16>; break;
+    case 32: ri = 0; break;
+    case 64: ri = 1; break;
+    case 128: ri = 2; break;
+    case 256: ri = 3; break;
     default: return -1;
   }
+  const void* fn = fns[ri][source];
   uint4 *out = nullptr, *src = nullptr;
   hipEvent_t a = nullptr, b = nullptr;
   hipError_t e = hipMalloc(&out, (size_t)blocks * kThreads * sizeof(uint4));
@@ -96,7 +124,7 @@ int dsa3d_probe_gather(int source, int row_bytes, int blocks, int iters, float* 
     void* args_lds[] = {(void*)&out, (void*)&iters, (void*)&seed};
     e = hipEventRecord(a, 0);
     if (e == hipSuccess)
-      e = hipLaunchKernel(fn, dim3(blocks), dim3(kThreads), source ? args_lds : args_l1, 0, 0);
+      e = hipLaunchKernel(fn, dim3(blocks), dim3(kThreads), source == 1 ? args_lds : args_l1, 0, 0);
     if (e == hipSuccess) e = hipEventRecord(b, 0);
     if (e == hipSuccess) e = hipEventSynchronize(b);
     if (e == hipSuccess) e = hipEventElapsedTime(ms, a, b);
