@@ -64,10 +64,13 @@ def workload_family(workload: str) -> str:
 
 
 def kernel_base(name: str) -> str:
-    """Kernel function name without namespace, template arguments or parameters."""
+    """Kernel function name without namespace, template arguments or parameters; the bf16
+    dK/dV gather (bwd_gather_mfma_kernel) under the name of the backward phase it runs,
+    bwd_gather_kernel."""
     import re
     m = re.search(r"(\w+_kernel)\b|(__amd_rocclr_copyBuffer)", name)
-    return m.group(0) if m else name[:60]
+    base = m.group(0) if m else name[:60]
+    return "bwd_gather_kernel" if base == "bwd_gather_mfma_kernel" else base
 
 
 def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
