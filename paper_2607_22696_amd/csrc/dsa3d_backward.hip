@@ -20,11 +20,12 @@
 //  3. finalize (one thread per point): d_offsets from A_p, B_p and the row's Delta; the
 //     point claims a slot of its bin from the cursor and writes its dK/dV coefficients
 //     (scale ds_p, alpha_p) and fractional position there, i.e. sorted by cell.
-//  4. gather (one L-lane group per 2 x 2 block of voxels in a frame): a voxel is corner c
-//     of exactly the points whose cell is voxel - c; for the block these bins form 6
-//     contiguous runs (cells x0-1, x0, x0+1 are adjacent), and the group accumulates
-//     w_c * coefficient * q and * dout rows in registers, then stores the dK and dV rows of
-//     its voxels once.
+//  4. gather: a voxel is corner c of exactly the points whose cell is voxel - c, so a block
+//     of voxels reads the bins of the cells around it, a few runs of adjacent bins, and
+//     stores the dK and dV rows of its voxels once.  bf16: one wave per 4 x 2 x 2 block, the
+//     sums as matrix products (weights x q / dout rows) on the matrix cores; fp32: one
+//     L-lane group per 2 x 2 block of a frame, w_c * coefficient * q and * dout accumulated
+//     in registers.
 #include "dsa3d_device.h"
 
 namespace dsa3d {
@@ -572,6 +573,7 @@ struct GatherLds {
   uint16_t q[PW ? 8 : kGB * D];  // the batch's rows, 16-byte chunks permuted per row
   uint16_t g[kGB * D];
   uint16_t a[PW ? 2 : 4][kGB * 16];  // A^T: (dV hi, dV lo[, dK hi, dK lo]), 32 rows of 16 bf16
+  int tok[kGB];     // the batch's query tokens, read by the lanes that copy their rows
   uint4 run[9][2];  // cell starts x0-1 .. x0+3 and the end, of the non-empty runs
   int rc[9];        // their cell row / plane: (y - y0 + 1) + 3 (z - z0 + 1)
 };
@@ -588,8 +590,11 @@ __device__ inline int gather_row_at(int e, int chunk) {
   else s = (e & 3) | (((e >> 3) & 1) << 2);
   return e * 2 * D + ((chunk ^ (2 * s)) << 4);
 }
-// A^T row e (32 bytes); rows 8..15 and 24..31 move to the other 128-byte half of the banks.
+// A^T row e (32 bytes); rows 8..15 and 24..31 move to the other 128-byte half of the banks,
+// and keep voxels 8..15 in their first 16 bytes and voxels 0..7 in the second, so that the
+// 16-byte writes of 16 consecutive rows (first half, then second) fall on distinct banks.
 __device__ inline int gather_at_at(int e) { return (e * 32) ^ (((e >> 3) & 1) << 7); }
+__device__ inline int gather_at_half(int e) { return ((e >> 3) & 1) << 4; }
 
 __device__ inline bf16x8_t tr_pair(const char* lo, const char* hi) {
   const s16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)lo);
@@ -610,7 +615,7 @@ __device__ inline bf16x8_t gather_b_frag(const uint16_t* rows, int db) {
 }
 __device__ inline bf16x8_t gather_a_frag(const uint16_t* at) {
   const int lane = threadIdx.x & 63, grp = lane >> 4, j = lane & 15;
-  const int e = 8 * grp + (j >> 2), in = (j & 3) * 8;
+  const int e = 8 * grp + (j >> 2), in = ((j & 3) * 8) ^ gather_at_half(e);
   const char* base = reinterpret_cast<const char*>(at);
   return tr_pair(base + gather_at_at(e) + in, base + gather_at_at(e + 4) + in);
 }
@@ -754,21 +759,23 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
       uint32_t hi[8], lo[8];
       weight_rows(i < d.end ? coef : 0.0f, fx, fy, fz, rcx, d.rc % 3 - 1, d.rc / 3 - 1, hi, lo);
       const int sel = upper ? 0 : 2;
+      const int h0 = gather_at_half(own), h1 = 16 - h0;  // bytes of voxels 0..7 and 8..15
       char* ah = reinterpret_cast<char*>(L.a[sel]) + gather_at_at(own);
       char* al = reinterpret_cast<char*>(L.a[sel + 1]) + gather_at_at(own);
-      *reinterpret_cast<uint4*>(ah) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-      *reinterpret_cast<uint4*>(ah + 16) = make_uint4(hi[4], hi[5], hi[6], hi[7]);
-      *reinterpret_cast<uint4*>(al) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      *reinterpret_cast<uint4*>(al + 16) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+      *reinterpret_cast<uint4*>(ah + h0) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+      *reinterpret_cast<uint4*>(ah + h1) = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+      *reinterpret_cast<uint4*>(al + h0) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      *reinterpret_cast<uint4*>(al + h1) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
     };
     uint4 rq[NI], rg[NI];
     bool part = false;  // the batch ends inside: its rows past the end are zeroed in LDS
     auto issue_rows = [&](const GatherPos& d, const GatherEntry& en) {
       part = d.end - d.u < (uint32_t)kGB;
+      if (lane < kGB) L.tok[lane] = (int)en.raw.x;  // lanes 0-31 hold n
 #pragma unroll
       for (int t = 0; t < NI; ++t) {
         const int e = lane / LPR + RPI * t;
-        const uint32_t n = (uint32_t)__shfl((int)en.raw.x, e);  // lanes 0-31 hold n
+        const uint32_t n = (uint32_t)L.tok[e];  // one dword per row, read by its LPR lanes
         const uint64_t o = (uint64_t)n * tok_bytes;
         if (d.u + e < d.end) {  // rows past the run's end are not loaded
           if constexpr (!PW) rq[t] = *reinterpret_cast<const uint4*>(qh + o);

@@ -117,8 +117,8 @@ SMALL_CASES = [
     small("grid_1x1x1", T=1, H=1, W=1, heads=2, head_dim=32, seed=21),
     small("t1_bf16", T=1, H=9, W=17, heads=2, head_dim=64, dtype="bf16", seed=22),
     small("w1_f32", T=6, H=7, W=1, heads=2, head_dim=32, seed=23),
-    # bf16 at head_dim 64 / 128 with up to 160 points runs the two-pass matrix-core forward;
-    # these cover its degenerate and mixed-size kernels and the fallback beyond 160 points
+    # bf16 with degenerate and mixed-size kernels (1 to 315 points) against the dK/dV
+    # matrix-core gather's 4 x 2 x 2 voxel blocks and 32-entry batches
     small("k111_bf16_d128", T=3, H=4, W=5, heads=2, head_dim=128, kt=1, kh=1, kw=1,
           dtype="bf16", seed=26),
     small("k135_bf16_d64", T=2, H=6, W=7, heads=3, head_dim=64, kt=1, kh=3, kw=5, dtype="bf16",
@@ -127,6 +127,11 @@ SMALL_CASES = [
           dtype="bf16", seed=28, offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
     small("k579_bf16_d64", T=5, H=7, W=9, heads=2, head_dim=64, kt=5, kh=7, kw=9, dtype="bf16",
           seed=29),
+    # grids thinner than one 4 x 2 x 2 gather block (a block with 2-4 cell columns, no second
+    # row or plane)
+    small("thin_bf16_d64", T=3, H=1, W=3, heads=2, head_dim=64, dtype="bf16", seed=50),
+    small("line_bf16_d32", T=2, H=2, W=1, heads=2, head_dim=32, dtype="bf16", seed=51),
+    small("grid_1x1x1_bf16_d128", T=1, H=1, W=1, heads=2, head_dim=128, dtype="bf16", seed=52),
     # 32 heads x 512-byte fp32 rows: a token's rows exceed the buffer record stride limit, so
     # every corner takes the global-load path
     small("wide_token_f32", T=2, H=4, W=5, heads=32, head_dim=128, seed=25,

@@ -68,6 +68,7 @@ SMALL = [
     small("pw_bf16_d128_3x5x5", T=4, H=7, W=9, heads=2, head_dim=128, dtype="bf16", kh=5, kw=5,
           seed=42, offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
     small("pw_f32_d64_1x3x3", T=3, H=10, W=6, heads=2, head_dim=64, dtype="f32", kt=1, seed=43),
+    small("pw_bf16_d32_thin", T=2, H=3, W=5, heads=2, head_dim=32, dtype="bf16", seed=44),
 ]
 
 
