@@ -650,8 +650,8 @@ __device__ inline void weight_rows(float c, float fx, float fy, float fz, int rc
   }
 }
 
-// A batch position: entries [u, min(u + 32, end)) of run r, whose cells x0 - 1 + i start at
-// m[i] (m[0] <= u); u >= end once the runs are exhausted.
+// A batch position: entries [u, min(u + 32, end)) of run r, whose cells x0 .. x0 + 3 start at
+// m1 .. m4 (cell x0 - 1 starts at or before u); u >= end once the runs are exhausted.
 struct GatherPos {
   uint32_t u, end, m1, m2, m3, m4;
   int rc, r;
