@@ -27,6 +27,8 @@
 // through the grid together) and keeps the plane's taps summed in registers; each wave writes
 // its sums to a workspace slot of its own, and a second kernel adds the slots in a fixed
 // order, so the weight gradients are deterministic and no float atomics are used.
+#include <type_traits>
+
 #include "dsa3d_device.h"
 #include "dsa3d_internal.h"
 
@@ -351,15 +353,21 @@ __device__ inline __attribute__((always_inline)) float2 bf16x2(uint32_t u) {
 }
 
 // out = conv(in) [+ bias] [+ out] for bf16 `in`; bricks ordered chunk, batch, row quad, strip.
+// The brick walks the input frames once: slice s (its rows and columns plus the filter halo)
+// sits in LDS buffer s & 1, each wave widens the KH rows it needs to fp32 once, and adds them
+// through filter plane a into output frame s + rt - a, for every a.  The KT output frames in
+// progress are held in registers (frame t in slot t % KT, the loop unrolled by KT so that the
+// slots are fixed registers); frame t is stored once slice t + rt has been added.
 template <bool OUT_BF16, bool FLIP, int KT, int KH, int KW>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2))) void dwconv_stream_kernel(
     ConvGeometry g, const void* __restrict__ in, const float* __restrict__ w,
     const float* __restrict__ bias, void* __restrict__ out, int accumulate, int bricks) {
   using RG = Ring<KT, KH, KW>;
-  __shared__ uint32_t ring[KT * RG::POS * 64];
+  static_assert(KT == 1 || KT == 3, "time extent 1 or 3");
+  __shared__ uint32_t slices[2][RG::POS * 64];
   constexpr int OS = OUT_BF16 ? 2 : 4;
+  constexpr int rt = (KT - 1) / 2;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rt = (KT - 1) / 2;
   const int frame_bytes = g.H * g.W * g.C * 2;  // below 2^31 on this path
   for (int brick = xcd_tile(blockIdx.x, gridDim.x); brick < bricks; brick += gridDim.x) {
     const int strip = brick % g.strips;
@@ -382,66 +390,87 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
     uint32_t off[RG::PER_WAVE];
     slice_offsets<KT, KH, KW>(g, i0, j0, c, wave, off);
     const char* base = static_cast<const char*>(in) + (int64_t)b * g.T * frame_bytes;
-    __syncthreads();  // the previous brick's last readers are done with the ring
-#pragma unroll 1
-    for (int f = -rt; f < rt; ++f) {
-      uint32_t v[RG::PER_WAVE];
-      load_slice<KT, KH, KW>(base, frame_bytes, f, g.T, off, v);
-      store_slice<KT, KH, KW>(ring, f, wave, lane, v);
-    }
-    uint32_t nxt[RG::PER_WAVE];
-    load_slice<KT, KH, KW>(base, frame_bytes, rt, g.T, off, nxt);
     char* obase = static_cast<char*>(out) + (int64_t)b * g.T * g.H * g.W * g.C * OS;
+
+    // While slice s is added, slot j holds output frame s - rt + j: plane a carries the slice
+    // into slot KT - 1 - a, slot 0 is then complete, and the slots shift down by one.
+    float2 acc[KT][kTok];
+#pragma unroll
+    for (int sl = 0; sl < KT; ++sl)
+#pragma unroll
+      for (int k = 0; k < kTok; ++k) acc[sl][k] = b2;
+    auto put = [&](int buf, const uint32_t (&v)[RG::PER_WAVE]) {
+#pragma unroll
+      for (int k = 0; k < RG::PER_WAVE; ++k) {
+        const int pos = wave + kWavesPerBlock * k;
+        if (pos < RG::POS) slices[buf][pos * 64 + lane] = v[k];
+      }
+    };
+    // stores output frame t (slot 0) of this wave's row
+    auto emit = [&](int t) {
+      if (!active || i >= g.H) return;
+      char* orow = obase + (((int64_t)t * g.H + i) * g.W) * g.C * OS + (int64_t)c * OS;
+#pragma unroll
+      for (int k = 0; k < kTok; ++k) {
+        if (j0 + k >= g.W) break;
+        char* o = orow + (int64_t)(j0 + k) * g.C * OS;
+        float2 v = acc[0][k];
+        if (accumulate) {
+          const float2 old = load2<OUT_BF16>(o);
+          v.x += old.x;
+          v.y += old.y;
+        }
+        if constexpr (OUT_BF16)
+          *reinterpret_cast<uint32_t*>(o) = bf16_bits(v.x) | (bf16_bits(v.y) << 16);
+        else
+          *reinterpret_cast<float2*>(o) = v;
+      }
+    };
+    uint32_t nxt[RG::PER_WAVE];
+    load_slice<KT, KH, KW>(base, frame_bytes, 0, g.T, off, nxt);
+    put(0, nxt);  // the previous brick ended on a barrier after its last read
+    if (g.T > 1) load_slice<KT, KH, KW>(base, frame_bytes, 1, g.T, off, nxt);
+    __syncthreads();
 #pragma unroll 1
-    for (int t = 0; t < g.T; ++t) {
-      store_slice<KT, KH, KW>(ring, t + rt, wave, lane, nxt);
-      __syncthreads();
-      load_slice<KT, KH, KW>(base, frame_bytes, t + rt + 1, g.T, off, nxt);
-      float2 acc[kTok];
+    for (int s = 0; s < g.T; ++s) {
+      // store slice s + 1, request slice s + 2, add slice s
+      if (s + 1 < g.T) {
+        put((s + 1) & 1, nxt);
+        if (s + 2 < g.T) load_slice<KT, KH, KW>(base, frame_bytes, s + 2, g.T, off, nxt);
+      }
+      const uint32_t* cur = slices[s & 1];
 #pragma unroll
-      for (int k = 0; k < kTok; ++k) acc[k] = b2;
+      for (int e = 0; e < KH; ++e) {
+        const uint32_t* src = cur + (wave + e) * RG::RX * 64 + lane;
+        float2 xv[RG::RX];
 #pragma unroll
-      for (int a = 0; a < KT; ++a) {
-        const int slot = ((t - rt + a) % KT + KT) % KT;
+        for (int x = 0; x < RG::RX; ++x) xv[x] = bf16x2(src[x * 64]);
 #pragma unroll
-        for (int e = 0; e < KH; ++e) {
-          const uint32_t* src = ring + (slot * RG::POS + (wave + e) * RG::RX) * 64 + lane;
-          float2 xv[RG::RX];
-#pragma unroll
-          for (int x = 0; x < RG::RX; ++x) xv[x] = bf16x2(src[x * 64]);
+        for (int a = 0; a < KT; ++a) {
+          if (s + rt - a >= g.T) continue;  // that output frame is past the end
 #pragma unroll
           for (int f = 0; f < KW; ++f) {
             const float2 wv = wt[(a * KH + e) * KW + f];
 #pragma unroll
             for (int k = 0; k < kTok; ++k) {
-              acc[k].x = fmaf(wv.x, xv[k + f].x, acc[k].x);
-              acc[k].y = fmaf(wv.y, xv[k + f].y, acc[k].y);
+              acc[KT - 1 - a][k].x = fmaf(wv.x, xv[k + f].x, acc[KT - 1 - a][k].x);
+              acc[KT - 1 - a][k].y = fmaf(wv.y, xv[k + f].y, acc[KT - 1 - a][k].y);
             }
           }
         }
-        // keep one plane's ring reads in flight at a time (register pressure)
-        asm volatile("" ::: "memory");
+        asm volatile("" ::: "memory");  // one row's reads in flight at a time (registers)
       }
-      if (active && i < g.H) {
-        char* orow = obase + (((int64_t)t * g.H + i) * g.W) * g.C * OS + (int64_t)c * OS;
+      if (s - rt >= 0) emit(s - rt);
 #pragma unroll
-        for (int k = 0; k < kTok; ++k) {
-          if (j0 + k >= g.W) break;
-          char* o = orow + (int64_t)(j0 + k) * g.C * OS;
-          float2 v = acc[k];
-          if (accumulate) {
-            const float2 old = load2<OUT_BF16>(o);
-            v.x += old.x;
-            v.y += old.y;
-          }
-          if constexpr (OUT_BF16)
-            *reinterpret_cast<uint32_t*>(o) = bf16_bits(v.x) | (bf16_bits(v.y) << 16);
-          else
-            *reinterpret_cast<float2*>(o) = v;
-        }
-      }
-      __syncthreads();  // every wave is done with the oldest slice before it is overwritten
+      for (int sl = 0; sl + 1 < KT; ++sl)
+#pragma unroll
+        for (int k = 0; k < kTok; ++k) acc[sl][k] = acc[sl + 1][k];
+#pragma unroll
+      for (int k = 0; k < kTok; ++k) acc[KT - 1][k] = b2;
+      __syncthreads();  // slice s is read; its buffer takes slice s + 2 next
     }
+    // frames T - rt .. T - 1 are complete after the last slice (slots 0 .. rt - 1)
+    if constexpr (rt == 1) emit(g.T - 1);
   }
 }
 
