@@ -476,15 +476,19 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
 
 // Weight and bias gradient partial sums on the streaming path: one brick per block; wave w of
 // brick (cc, b, iq, strip) writes slot ((b * hq + iq) * strips + strip) * 4 + w, its sums
-// over all frames of its row of the brick.
+// over all frames of its row of the brick.  As in the forward, the x slices are walked once
+// (LDS buffer s & 1, each row widened once per wave): slice s meets dy frame s + rt - a through
+// filter plane a, and the KT dy frames in use are held in registers (slot j: frame s - rt + j),
+// shifting down by one per slice.
 template <int KT, int KH, int KW>
 __global__ __launch_bounds__(kBlockThreads) void dwconv_stream_wgrad_kernel(
     ConvGeometry g, const void* __restrict__ x, const void* __restrict__ dy,
     float* __restrict__ part, float* __restrict__ part_b) {
   using RG = Ring<KT, KH, KW>;
-  __shared__ uint32_t ring[KT * RG::POS * 64];
+  static_assert(KT == 1 || KT == 3, "time extent 1 or 3");
+  __shared__ uint32_t slices[2][RG::POS * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rt = (KT - 1) / 2;
+  constexpr int rt = (KT - 1) / 2;
   const int frame_bytes = g.H * g.W * g.C * 2;  // below 2^31 on this path
   const int brick = xcd_tile(blockIdx.x, gridDim.x);
   const int strip = brick % g.strips;
@@ -506,62 +510,83 @@ __global__ __launch_bounds__(kBlockThreads) void dwconv_stream_wgrad_kernel(
                   : 0xffffffffu;
   const char* xbase = static_cast<const char*>(x) + (int64_t)b * g.T * frame_bytes;
   const char* dbase = static_cast<const char*>(dy) + (int64_t)b * g.T * frame_bytes;
+  auto load_dy = [&](int f, uint32_t (&v)[kTok]) {  // zeros outside [0, T)
+    const __amdgpu_buffer_rsrc_t rs = frame_rsrc(dbase, frame_bytes, f, g.T);
+#pragma unroll
+    for (int k = 0; k < kTok; ++k) v[k] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, (int)doff[k], 0, 0);
+  };
+  auto put = [&](int buf, const uint32_t (&v)[RG::PER_WAVE]) {
+#pragma unroll
+    for (int k = 0; k < RG::PER_WAVE; ++k) {
+      const int pos = wave + kWavesPerBlock * k;
+      if (pos < RG::POS) slices[buf][pos * 64 + lane] = v[k];
+    }
+  };
   float2 acc[RG::TAPS];
 #pragma unroll
   for (int tap = 0; tap < RG::TAPS; ++tap) acc[tap] = make_float2(0.0f, 0.0f);
   float2 db = make_float2(0.0f, 0.0f);
-#pragma unroll 1
-  for (int f = -rt; f < rt; ++f) {
-    uint32_t v[RG::PER_WAVE];
-    load_slice<KT, KH, KW>(xbase, frame_bytes, f, g.T, off, v);
-    store_slice<KT, KH, KW>(ring, f, wave, lane, v);
-  }
-  uint32_t nxt[RG::PER_WAVE], dnxt[kTok];
-  load_slice<KT, KH, KW>(xbase, frame_bytes, rt, g.T, off, nxt);
-  {
-    const __amdgpu_buffer_rsrc_t r = frame_rsrc(dbase, frame_bytes, 0, g.T);
+  // dy window: slot j = frame s - rt + j (frames below 0 are zero)
+  float2 d[KT][kTok];
 #pragma unroll
-    for (int k = 0; k < kTok; ++k) dnxt[k] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)doff[k], 0, 0);
-  }
-#pragma unroll 1
-  for (int t = 0; t < g.T; ++t) {
-    store_slice<KT, KH, KW>(ring, t + rt, wave, lane, nxt);
-    __syncthreads();
-    float2 d[kTok];
-#pragma unroll
-    for (int k = 0; k < kTok; ++k) d[k] = bf16x2(dnxt[k]);
-    load_slice<KT, KH, KW>(xbase, frame_bytes, t + rt + 1, g.T, off, nxt);
-    {
-      const __amdgpu_buffer_rsrc_t r = frame_rsrc(dbase, frame_bytes, t + 1, g.T);
-#pragma unroll
-      for (int k = 0; k < kTok; ++k)
-        dnxt[k] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)doff[k], 0, 0);
-    }
+  for (int j = 0; j < KT; ++j) {
+    uint32_t v[kTok];
+    load_dy(j - rt, v);
 #pragma unroll
     for (int k = 0; k < kTok; ++k) {
-      db.x += d[k].x;
-      db.y += d[k].y;
+      d[j][k] = bf16x2(v[k]);
+      if (j >= rt) {  // frames 0 .. rt enter the bias sum here, later ones as they arrive
+        db.x += d[j][k].x;
+        db.y += d[j][k].y;
+      }
     }
+  }
+  uint32_t dnxt[kTok];
+  load_dy(rt + 1, dnxt);
+  uint32_t nxt[RG::PER_WAVE];
+  load_slice<KT, KH, KW>(xbase, frame_bytes, 0, g.T, off, nxt);
+  put(0, nxt);
+  if (g.T > 1) load_slice<KT, KH, KW>(xbase, frame_bytes, 1, g.T, off, nxt);
+  __syncthreads();
+#pragma unroll 1
+  for (int s = 0; s < g.T; ++s) {
+    if (s + 1 < g.T) {
+      put((s + 1) & 1, nxt);
+      if (s + 2 < g.T) load_slice<KT, KH, KW>(xbase, frame_bytes, s + 2, g.T, off, nxt);
+    }
+    const uint32_t* cur = slices[s & 1];
 #pragma unroll
-    for (int a = 0; a < KT; ++a) {
-      const int slot = ((t - rt + a) % KT + KT) % KT;
+    for (int e = 0; e < KH; ++e) {
+      const uint32_t* src = cur + (wave + e) * RG::RX * 64 + lane;
+      float2 xv[RG::RX];
 #pragma unroll
-      for (int e = 0; e < KH; ++e) {
-        const uint32_t* src = ring + (slot * RG::POS + (wave + e) * RG::RX) * 64 + lane;
-        float2 xv[RG::RX];
+      for (int q = 0; q < RG::RX; ++q) xv[q] = bf16x2(src[q * 64]);
 #pragma unroll
-        for (int q = 0; q < RG::RX; ++q) xv[q] = bf16x2(src[q * 64]);
+      for (int a = 0; a < KT; ++a) {
 #pragma unroll
         for (int f = 0; f < KW; ++f)
 #pragma unroll
           for (int k = 0; k < kTok; ++k) {
-            acc[(a * KH + e) * KW + f].x = fmaf(d[k].x, xv[k + f].x, acc[(a * KH + e) * KW + f].x);
-            acc[(a * KH + e) * KW + f].y = fmaf(d[k].y, xv[k + f].y, acc[(a * KH + e) * KW + f].y);
+            const float2 dv = d[KT - 1 - a][k];  // dy frame s + rt - a (zero outside the grid)
+            acc[(a * KH + e) * KW + f].x = fmaf(dv.x, xv[k + f].x, acc[(a * KH + e) * KW + f].x);
+            acc[(a * KH + e) * KW + f].y = fmaf(dv.y, xv[k + f].y, acc[(a * KH + e) * KW + f].y);
           }
       }
-      asm volatile("" ::: "memory");  // one plane's ring reads in flight at a time
+      asm volatile("" ::: "memory");  // one row's reads in flight at a time (registers)
     }
-    __syncthreads();
+    // shift the dy window; frame s + rt + 1 enters (and the bias sum)
+#pragma unroll
+    for (int j = 0; j + 1 < KT; ++j)
+#pragma unroll
+      for (int k = 0; k < kTok; ++k) d[j][k] = d[j + 1][k];
+#pragma unroll
+    for (int k = 0; k < kTok; ++k) {
+      d[KT - 1][k] = bf16x2(dnxt[k]);
+      db.x += d[KT - 1][k].x;
+      db.y += d[KT - 1][k].y;
+    }
+    load_dy(s + rt + 2, dnxt);
+    __syncthreads();  // slice s is read; its buffer takes slice s + 2 next
   }
   if (!active) return;
   const int64_t slot = (((int64_t)b * g.hq + iq) * g.strips + strip) * kWavesPerBlock + wave;

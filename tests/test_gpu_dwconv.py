@@ -63,6 +63,12 @@ SMALL = [
     conv("f32_9x1x1", 1, 10, 2, 9, 4, (9, 1, 1), "f32", 34),
     conv("bf16_narrow_W3", 2, 2, 1, 3, 2, (3, 3, 3), "bf16", 35),
     conv("f32_1x7x7_T1", 1, 1, 9, 10, 20, (1, 7, 7), "f32", 36),
+    # the bf16 streaming path (every extent 1 or 3) with a time extent of 1, a single frame,
+    # mixed extents, a 1 x 1 x 1 filter, two batch items and a ragged channel chunk
+    conv("bf16_1x3x3_B2_C130", 2, 3, 6, 10, 130, (1, 3, 3), "bf16", 37),
+    conv("bf16_3x1x3_T1", 1, 1, 5, 9, 128, (3, 1, 3), "bf16", 38),
+    conv("bf16_3x3x1_T2", 1, 2, 7, 5, 64, (3, 3, 1), "bf16", 39),
+    conv("bf16_1x1x1", 1, 3, 4, 5, 32, (1, 1, 1), "bf16", 40),
 ]
 
 
