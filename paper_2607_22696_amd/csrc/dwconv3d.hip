@@ -93,6 +93,11 @@ __device__ inline void stage_weights(const ConvGeometry& g, const float* __restr
 
 // out = conv(in) [+ bias] [+ out]; FLIP reverses the filter (the transposed convolution).
 // Tiles are numbered chunk-major: tile = (cc * B + b) * g.tiles_per_bc + q.
+// Two fp32 values rounded to nearest even as a bf16 pair (v_cvt_pk_bf16_f32), x in the low half.
+__device__ inline __attribute__((always_inline)) uint32_t pack_bf16x2(float x, float y) {
+  return __builtin_bit_cast(uint32_t, bf16x2_t{(__bf16)x, (__bf16)y});
+}
+
 template <bool IN_BF16, bool OUT_BF16, bool FLIP, int KW>
 __global__ __launch_bounds__(kBlockThreads) void dwconv_kernel(ConvGeometry g,
                                                                const void* __restrict__ in,
@@ -165,7 +170,7 @@ __global__ __launch_bounds__(kBlockThreads) void dwconv_kernel(ConvGeometry g,
         v.y += old.y;
       }
       if constexpr (OUT_BF16)
-        *reinterpret_cast<uint32_t*>(o) = bf16_bits(v.x) | (bf16_bits(v.y) << 16);
+        *reinterpret_cast<uint32_t*>(o) = pack_bf16x2(v.x, v.y);
       else
         *reinterpret_cast<float2*>(o) = v;
     }
@@ -421,7 +426,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
           v.y += old.y;
         }
         if constexpr (OUT_BF16)
-          *reinterpret_cast<uint32_t*>(o) = bf16_bits(v.x) | (bf16_bits(v.y) << 16);
+          *reinterpret_cast<uint32_t*>(o) = pack_bf16x2(v.x, v.y);
         else
           *reinterpret_cast<float2*>(o) = v;
       }
