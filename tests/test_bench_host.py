@@ -1,0 +1,82 @@
+"""Host-side logic of bench.py (CPU only): roofline classification, kernel-name mapping, the
+algorithmic byte and FLOP counts per launch, the one-GPU rule and the gather probe's argument
+checks."""
+import ctypes
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+import testgen  # noqa: E402
+
+
+def test_roofline_takes_the_slower_of_memory_and_arithmetic():
+    # 8e9 bytes take 1 ms at 8 TB/s; 1e9 flops take 6.4 us at 157.3 TFLOP/s: HBM-bound
+    r = bench.roofline({"bytes": 8e9, "flops": 1e9}, 2.0)
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s"
+    assert r["achieved"] == pytest.approx(4000.0) and r["frac"] == pytest.approx(0.5)
+    # 1.573e12 flops take 10 ms at the fp32 vector peak; 8e9 bytes 1 ms: ALU-bound
+    r = bench.roofline({"bytes": 8e9, "flops": 1.573e12}, 20.0)
+    assert r["bound"] == "alu" and r["peak"] == bench.VALU_PEAK_TFLOPS
+    assert r["frac"] == pytest.approx(0.5, rel=1e-3)
+
+
+def test_the_bf16_gather_is_priced_against_the_matrix_peak():
+    w16 = testgen.WORKLOADS["fwdbwd_64x34x60"]
+    alg = bench.algorithmic(w16)
+    g = bench.kernel_roofline(w16, alg, "bwd_gather_kernel", 3.0)
+    # 32 P D flops per row against 2.5 PFLOP/s take less time than the HBM bytes at 8 TB/s
+    assert g["bound"] == "hbm"
+    assert bench.kernel_roofline(w16, alg, "bwd_sweep_kernel", 6.0)["bound"] == "alu"
+    w32 = testgen.WORKLOADS["tiny_f32"]
+    a32 = bench.algorithmic(w32)
+    assert bench.kernel_roofline(w32, a32, "bwd_gather_kernel", 1.0) == bench.roofline(
+        a32["bwd_gather_kernel"], 1.0)
+
+
+def test_kernel_names_map_to_the_phases_the_bench_times():
+    assert bench.kernel_base("void dsa3d::(anonymous namespace)::fwd_kernel<64, true, false>"
+                             "(dsa3d::Geometry, ...)") == "fwd_kernel"
+    assert bench.kernel_base("dsa3d::bwd_gather_mfma_kernel<64, false>(...)") == "bwd_gather_kernel"
+    assert bench.kernel_base("dsa3d::bwd_gather_kernel<32, false, false>(...)") == "bwd_gather_kernel"
+    assert bench.kernel_base("__amd_rocclr_copyBuffer") == "__amd_rocclr_copyBuffer"
+
+
+def test_algorithmic_counts_follow_the_documented_per_row_formulas():
+    w = testgen.WORKLOADS["tiny_f32"]  # 512 rows, P = 27, D = 32, fp32
+    rows, P, D, s = w.queries, w.P, w.head_dim, 4
+    alg = bench.algorithmic(w)
+    assert alg["fwd_kernel"]["bytes"] == rows * (4 * D * s + 12 * P + 4)
+    assert alg["fwd_kernel"]["flops"] == rows * 32 * P * D
+    assert alg["bwd_gather_kernel"]["bytes"] == rows * (2 * D * s + 8 * D)
+    assert alg["backward"]["flops"] == rows * 80 * P * D
+    vm = bench.vmem_bytes(w)
+    assert vm["fwd_kernel"] == rows * (16 * P * D * s + 2 * D * s + 12 * P + 4)
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
+
+
+def test_gather_probe_rejects_bad_arguments_before_touching_the_device():
+    path = os.path.join(ROOT, "paper_2607_22696_amd", "libdsa3d_probe.so")
+    if not os.path.exists(path):
+        pytest.skip("probe library not built")
+    lib = ctypes.CDLL(path)
+    fn = lib.dsa3d_probe_gather
+    fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                   ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]
+    ms, nb = ctypes.c_float(), ctypes.c_double()
+    assert fn(3, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no such source
+    assert fn(-1, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1
+    assert fn(2, 48, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1    # row size
+    assert fn(0, 128, 0, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no blocks
+    assert fn(1, 64, 8, 8, None, ctypes.byref(nb)) == -1                # null output
