@@ -288,14 +288,14 @@ __global__ __launch_bounds__(kBlockThreads) void dwconv_wgrad_reduce_kernel(
 // ---------------------------------------------------------------------------- time streaming
 
 // Fast path for bf16 data and filters of at most 3 along every axis.  A block owns a brick of
-// 4 grid rows x 8 tokens x 128 channels and walks all frames.  The last KT input slices of the
-// brick (its rows and columns plus the filter's halo, zero outside the grid) sit in an LDS
-// ring; each step stores the next frame's slice, prefetches the one after into registers, and
-// computes the brick's outputs for one frame from the ring, so every input element comes from
-// HBM about once (the halo columns and rows are re-read, mostly from L2, by the neighbouring
-// bricks, which walk the frames at the same time).  The filter taps are in registers.
+// 4 grid rows x 8 tokens x 128 channels and walks all frames.  One input slice of the brick (its
+// rows and columns plus the filter's halo, zero outside the grid) is staged per frame, in one of
+// two LDS buffers; while a slice is used, the next one is stored into the other buffer and the
+// one after that is in flight into registers, so every input element comes from HBM about once
+// (the halo columns and rows are re-read, mostly from L2, by the neighbouring bricks, which walk
+// the frames at the same time).  The filter taps are in registers.
 template <int KT, int KH, int KW>
-struct Ring {
+struct SliceShape {
   static constexpr int RY = kRows + KH - 1;  // slice rows
   static constexpr int RX = kTok + KW - 1;   // slice columns
   static constexpr int POS = RY * RX;        // token positions per slice
@@ -307,8 +307,8 @@ struct Ring {
 // buffer unit reads as zero, outside the grid or the channel range), computed once per brick.
 template <int KT, int KH, int KW>
 __device__ inline void slice_offsets(const ConvGeometry& g, int i0, int j0, int c, int wave,
-                                     uint32_t (&off)[Ring<KT, KH, KW>::PER_WAVE]) {
-  using RG = Ring<KT, KH, KW>;
+                                     uint32_t (&off)[SliceShape<KT, KH, KW>::PER_WAVE]) {
+  using RG = SliceShape<KT, KH, KW>;
   const int rh = (KH - 1) / 2, rw = (KW - 1) / 2;
 #pragma unroll
   for (int k = 0; k < RG::PER_WAVE; ++k) {
@@ -334,23 +334,11 @@ __device__ inline __attribute__((always_inline)) __amdgpu_buffer_rsrc_t frame_rs
 template <int KT, int KH, int KW>
 __device__ inline __attribute__((always_inline)) void load_slice(
     const char* batch_base, int frame_bytes, int f, int T,
-    const uint32_t (&off)[Ring<KT, KH, KW>::PER_WAVE], uint32_t (&v)[Ring<KT, KH, KW>::PER_WAVE]) {
+    const uint32_t (&off)[SliceShape<KT, KH, KW>::PER_WAVE], uint32_t (&v)[SliceShape<KT, KH, KW>::PER_WAVE]) {
   const __amdgpu_buffer_rsrc_t r = frame_rsrc(batch_base, frame_bytes, f, T);
 #pragma unroll
-  for (int k = 0; k < Ring<KT, KH, KW>::PER_WAVE; ++k)
+  for (int k = 0; k < SliceShape<KT, KH, KW>::PER_WAVE; ++k)
     v[k] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off[k], 0, 0);
-}
-
-template <int KT, int KH, int KW>
-__device__ inline __attribute__((always_inline)) void store_slice(
-    uint32_t* ring, int f, int wave, int lane, const uint32_t (&v)[Ring<KT, KH, KW>::PER_WAVE]) {
-  using RG = Ring<KT, KH, KW>;
-  const int slot = ((f % KT) + KT) % KT;
-#pragma unroll
-  for (int k = 0; k < RG::PER_WAVE; ++k) {
-    const int pos = wave + kWavesPerBlock * k;
-    if (pos < RG::POS) ring[(slot * RG::POS + pos) * 64 + lane] = v[k];
-  }
 }
 
 __device__ inline __attribute__((always_inline)) float2 bf16x2(uint32_t u) {
@@ -361,13 +349,13 @@ __device__ inline __attribute__((always_inline)) float2 bf16x2(uint32_t u) {
 // The brick walks the input frames once: slice s (its rows and columns plus the filter halo)
 // sits in LDS buffer s & 1, each wave widens the KH rows it needs to fp32 once, and adds them
 // through filter plane a into output frame s + rt - a, for every a.  The KT output frames in
-// progress are held in registers (frame t in slot t % KT, the loop unrolled by KT so that the
-// slots are fixed registers); frame t is stored once slice t + rt has been added.
+// progress are held in registers and shift down by one slot per slice; frame t is stored once
+// slice t + rt has been added.
 template <bool OUT_BF16, bool FLIP, int KT, int KH, int KW>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2))) void dwconv_stream_kernel(
     ConvGeometry g, const void* __restrict__ in, const float* __restrict__ w,
     const float* __restrict__ bias, void* __restrict__ out, int accumulate, int bricks) {
-  using RG = Ring<KT, KH, KW>;
+  using RG = SliceShape<KT, KH, KW>;
   static_assert(KT == 1 || KT == 3, "time extent 1 or 3");
   __shared__ uint32_t slices[2][RG::POS * 64];
   constexpr int OS = OUT_BF16 ? 2 : 4;
@@ -489,7 +477,7 @@ template <int KT, int KH, int KW>
 __global__ __launch_bounds__(kBlockThreads) void dwconv_stream_wgrad_kernel(
     ConvGeometry g, const void* __restrict__ x, const void* __restrict__ dy,
     float* __restrict__ part, float* __restrict__ part_b) {
-  using RG = Ring<KT, KH, KW>;
+  using RG = SliceShape<KT, KH, KW>;
   static_assert(KT == 1 || KT == 3, "time extent 1 or 3");
   __shared__ uint32_t slices[2][RG::POS * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
