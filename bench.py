@@ -784,7 +784,8 @@ def main():
         if n in kernel_ms:
             tbps = b / (kernel_ms[n] * 1e-3) / 1e12
             gather_path[n] = {"bytes_per_launch": b, "achieved_TBps": round(tbps, 2),
-                              "frac_of_l1_ceiling": round(tbps / ceil["l1_TBps"], 3)}
+                              "frac_of_l1_ceiling": round(tbps / ceil["l1_TBps"], 3),
+                              "frac_of_l2_ceiling": round(tbps / ceil["l2_TBps"], 3)}
 
     res = {
         "metric": METRIC,
