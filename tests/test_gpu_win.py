@@ -164,7 +164,10 @@ def test_swin_64x34x60_full_size():
         check(f"dv[{t0}:{t1}]", to_host(dv[:, t0:t1]), rdv)
 
 
+# 51 GB of bf16 inputs are generated on the host and two 3-frame backward regions go
+# through the fp64 oracle: about two minutes of host work besides the GPU run.
 @pytest.mark.slow
+@pytest.mark.timeout(420)
 def test_swin_1080p_256f_full_size():
     """2,088,960 tokens x 24 heads x 128, shifted 3 x 16 x 16 windows (Swin-DiT's attention on
     256 frames of 1080p): the launch configuration the bench times; out and lse on the first, a
