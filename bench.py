@@ -125,6 +125,36 @@ def measured_traffic(workload, kernel):
     return None if k is None else k["hbm_bytes"]
 
 
+# kernels of one backward call, in launch order (the bin scan is four small kernels)
+BWD_KERNELS = ("bwd_sweep_kernel", "fill_u32_kernel", "scan_reduce_kernel", "scan_sums_kernel",
+               "scan_apply_kernel", "bwd_finalize_kernel", "bwd_gather_kernel")
+
+
+def measured_step_traffic(workload, backward):
+    """HBM bytes of one step (forward, and the backward's kernels if `backward`) summed from
+    profiles/traffic_<workload>.json, or None if the file is absent, was taken from other
+    kernel sources, or lacks one of the step's kernels."""
+    names = ("fwd_kernel",) + (BWD_KERNELS if backward else ())
+    total = 0
+    for n in names:
+        b = measured_traffic(workload, n)
+        if b is None:
+            return None
+        total += b
+    return total
+
+
+def hbm_rocprof(workload, backward, ms_step):
+    """The step's HBM traffic as rocprofv3 counted it (FETCH_SIZE + WRITE_SIZE, calibrated on
+    a device copy) over the step time measured in this run: GB/s and fraction of the 8 TB/s
+    peak, or None where no counters for the current kernel sources are committed."""
+    b = measured_step_traffic(workload, backward)
+    if b is None:
+        return None
+    gbs = b / (ms_step * 1e-3) / 1e9
+    return {"bytes_per_step": b, "GBps": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 def algorithmic(w):
     """Algorithmic HBM bytes and FLOPs per launch of each kernel, and of the two entry points.
 
@@ -812,6 +842,7 @@ def main():
         "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "token_head_rows_per_s": round(w.queries / (ms_step * 1e-3), 1),
         "roofline": roof,
+        "hbm_rocprof": hbm_rocprof(w.name, do_bwd, ms_step),
         "gather_path": gather_path,
         "input_gen_s": round(t_gen, 1),
     }

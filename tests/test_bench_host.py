@@ -1,6 +1,6 @@
 """Host-side logic of bench.py (CPU only): roofline classification, kernel-name mapping, the
-algorithmic byte and FLOP counts per launch, the one-GPU rule and the gather probe's argument
-checks."""
+algorithmic byte and FLOP counts per launch, the rocprof-counted step traffic, the one-GPU rule
+and the gather probe's argument checks."""
 import ctypes
 import os
 import subprocess
@@ -80,3 +80,27 @@ def test_gather_probe_rejects_bad_arguments_before_touching_the_device():
     assert fn(2, 48, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1    # row size
     assert fn(0, 128, 0, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no blocks
     assert fn(1, 64, 8, 8, None, ctypes.byref(nb)) == -1                # null output
+
+
+def test_rocprof_step_traffic_sums_the_step_kernels_and_refuses_stale_counters(tmp_path, monkeypatch):
+    import json
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    names = ("fwd_kernel",) + bench.BWD_KERNELS
+    kernels = {n: {"hbm_bytes": 10 ** i} for i, n in enumerate(names)}
+    doc = {"workload": "w", "kernel_source_hash": bench.kernel_source_hash("dsa"), "kernels": kernels}
+    (tmp_path / "traffic_w.json").write_text(json.dumps(doc))
+    assert bench.measured_step_traffic("w", False) == 1
+    assert bench.measured_step_traffic("w", True) == 11111111
+    # 8e9 bytes in 1 ms is the 8 TB/s peak
+    kernels["fwd_kernel"]["hbm_bytes"] = 8 * 10 ** 9
+    (tmp_path / "traffic_w.json").write_text(json.dumps(doc))
+    r = bench.hbm_rocprof("w", False, 1.0)
+    assert r["GBps"] == pytest.approx(8000.0) and r["frac_of_peak"] == pytest.approx(1.0)
+    # a kernel of the step without counters, counters of other sources, no file: no figure
+    del kernels["bwd_finalize_kernel"]
+    (tmp_path / "traffic_w.json").write_text(json.dumps(doc))
+    assert bench.measured_step_traffic("w", True) is None
+    doc["kernel_source_hash"] = "0" * 16
+    (tmp_path / "traffic_w.json").write_text(json.dumps(doc))
+    assert bench.hbm_rocprof("w", False, 1.0) is None
+    assert bench.hbm_rocprof("absent", True, 1.0) is None
