@@ -103,7 +103,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const int khw = g.kh * g.kw;
 
-  for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
+  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
+       tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
     const int n0 = (tile % tiles_per_bh) * LY::kRowsPerBlock;
@@ -478,7 +479,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_
   const int tiles_per_bh = (Nb + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   const uint32_t tok_bytes = (uint32_t)g.heads * LY::kRowBytes;  // one token's rows, all heads
 
-  for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
+  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
+       tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
     const int nb = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
@@ -685,7 +687,8 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
   const bool upper = lane >= 32;  // dV coefficients (else dK)
   const int own = lane & 31;      // the entry whose coefficients this lane forms
 
-  for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
+  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
+       tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int blk = (tile % tiles_per_bh) * NW + wave;
     if (blk >= nblk) continue;

@@ -11,8 +11,9 @@
 // its LSE are stored once.
 //
 // Memory order: consecutive workgroups go to the 8 XCDs round-robin; blocks are renumbered
-// so each XCD walks one contiguous range of (batch, head, token) tiles and its L2 holds one
-// head's sliding band of K/V rows.
+// so that each XCD walks contiguous runs of (batch, head, token) tiles while the eight XCDs
+// work on neighbouring runs of one head, sharing that head's band of K/V rows in the
+// memory-side cache.
 #include "dsa3d_device.h"
 
 namespace dsa3d {
@@ -46,7 +47,8 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const int khw = g.kh * g.kw;
 
-  for (int tile = xcd_tile(blockIdx.x, gridDim.x); tile < tiles; tile += gridDim.x) {
+  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
+       tile += gridDim.x) {
     const int bh = tile / tiles_per_bh;
     const int b = bh / g.heads, m = bh % g.heads;
     const int n0 = (tile % tiles_per_bh) * LY::kRowsPerBlock;
