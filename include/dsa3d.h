@@ -28,7 +28,7 @@
  *  - Every data pointer is a DEVICE pointer on the current HIP device, owned
  *    by the caller.  The library never allocates, frees, synchronises or
  *    prints, and keeps no mutable global state; calls are thread-safe.
- *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ *  - Work is enqueued on `stream` (NULL = the null stream).
  *    DSA3D_OK means "validated and enqueued"; a fault during execution shows
  *    up at the caller's next synchronisation.
  *  - All arguments are validated on the host before anything is enqueued.  On
@@ -45,6 +45,7 @@
 #ifndef DSA3D_H
 #define DSA3D_H
 
+#include <hip/hip_runtime_api.h> /* hipStream_t, hipEvent_t */
 #include <stddef.h>
 #include <stdint.h>
 
@@ -60,8 +61,8 @@ typedef enum {
   DSA3D_ERR_UNSUPPORTED = 3,   /* dtype or head_dim not built in, or P > DSA3D_MAX_POINTS  */
   DSA3D_ERR_MISALIGNED = 4,    /* a pointer breaks the alignment rule above               */
   DSA3D_ERR_WORKSPACE = 5,     /* workspace NULL or smaller than the required size        */
-  DSA3D_ERR_ALIAS = 6,         /* an output overlaps an input or another output           */
-  DSA3D_ERR_DEVICE = 7         /* a HIP launch failed (the HIP error is not cleared)      */
+  DSA3D_ERR_DEVICE = 6,        /* a HIP launch failed (the HIP error is not cleared)      */
+  DSA3D_ERR_ALIAS = 7          /* an output overlaps an input or another output           */
 } dsa3d_status;
 
 typedef enum { DSA3D_F32 = 0, DSA3D_BF16 = 1 } dsa3d_dtype;
@@ -92,7 +93,7 @@ typedef struct {
  *             for inference.
  * Accumulation is fp32 for both dtypes. */
 dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
-                           const float* offsets, void* out, float* lse, void* stream);
+                           const float* offsets, void* out, float* lse, hipStream_t stream);
 
 /* Bytes of device workspace dsa3d_backward needs for `desc`: about 56 bytes per
  * (query row, point) pair plus 12 bytes per trilinear cell.  Returns 0 for a descriptor that
@@ -106,8 +107,12 @@ size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc);
  *   d_offsets[p] = sum_c (d w_c / d pos) (scale ds_p <q, K[c]> + alpha_p <dout, V[c]>)
  * summed over the trilinear corners c of every point (w_c its weight, zero-padded corners
  * skipped).  At an exact integer coordinate the floor-based (upper one-sided) derivative is
- * used.  alpha_p is recomputed from `lse` and Delta from the recomputed alpha_p and da_p, so
- * the forward output itself is not needed.
+ * used.  alpha_p is recomputed from `lse`.
+ *   out      : the forward's output for the same inputs, or NULL.  It is not read: Delta is
+ *              formed exactly from the recomputed alpha_p and da_p while the points are swept
+ *              (it equals <dout, out> up to the rounding of out to its storage type, which
+ *              for bf16 would cost about 2^-9 of Delta).  When given it must be 16-byte
+ *              aligned and must not overlap an output or the workspace.
  *   lse      : the forward's LSE for the same inputs.
  *   dout     : upstream gradient of out (descriptor dtype).
  *   dq, d_offsets : fully overwritten.
@@ -123,9 +128,9 @@ size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc);
  * below 2^31 (DSA3D_ERR_INVALID_SHAPE otherwise).
  * Accumulation is fp32. */
 dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
-                            const float* offsets, const float* lse, const void* dout, float* dq,
-                            float* dk, float* dv, float* d_offsets, void* workspace,
-                            size_t workspace_bytes, void* stream);
+                            const float* offsets, const void* out, const float* lse,
+                            const void* dout, float* dq, float* dk, float* dv, float* d_offsets,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Phases of dsa3d_backward, in launch order: 0 the sweep over query rows (dq, per-point
  * records, bin counts), 1 the exclusive scan of the bin counts, 2 the pass over points
@@ -133,16 +138,17 @@ dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k
 #define DSA3D_BACKWARD_PHASES 4
 
 /* dsa3d_backward with phase timing, for benchmarks and profilers.  `events` is NULL or
- * points to DSA3D_BACKWARD_PHASES + 1 HIP events (hipEvent_t handles, created by the caller
- * on the current device and owned by it); event i is recorded on `stream` right before
- * phase i is launched and the last one after the last phase, so the time between events i
- * and i + 1 is phase i alone.  Arguments, checks and results are those of dsa3d_backward;
- * a failed event record returns DSA3D_ERR_DEVICE. */
+ * points to DSA3D_BACKWARD_PHASES + 1 HIP events (created by the caller on the current
+ * device and owned by it); event i is recorded on `stream` right before phase i is launched
+ * and the last one after the last phase, so the time between events i and i + 1 is phase i
+ * alone.  Arguments, checks and results are those of dsa3d_backward; a failed event record
+ * returns DSA3D_ERR_DEVICE. */
 dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const void* k,
-                                  const void* v, const float* offsets, const float* lse,
-                                  const void* dout, float* dq, float* dk, float* dv,
-                                  float* d_offsets, void* workspace, size_t workspace_bytes,
-                                  void* stream, void* const* events);
+                                  const void* v, const float* offsets, const void* out,
+                                  const float* lse, const void* dout, float* dq, float* dk,
+                                  float* dv, float* d_offsets, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream,
+                                  const hipEvent_t* events);
 
 /* Static description of a status code (never NULL). */
 const char* dsa3d_status_string(dsa3d_status status);

@@ -58,7 +58,7 @@ typedef struct {
  * overlapping x, weight or bias -> DSA3D_ERR_ALIAS. */
 dsa3d_status dsa3d_dwconv3d_forward(const dsa3d_dwconv_desc* desc, const void* x,
                                     const float* weight, const float* bias, void* y,
-                                    int accumulate, void* stream);
+                                    int accumulate, hipStream_t stream);
 
 /* Bytes of device workspace dsa3d_dwconv3d_backward needs for the weight and bias gradients
  * (partial sums of the grid sweep: 4 bytes per channel and tap, and per channel, for each of
@@ -81,7 +81,7 @@ size_t dsa3d_dwconv3d_backward_workspace_size(const dsa3d_dwconv_desc* desc);
 dsa3d_status dsa3d_dwconv3d_backward(const dsa3d_dwconv_desc* desc, const void* x,
                                      const float* weight, const void* dy, float* dx,
                                      int accumulate_dx, float* dweight, float* dbias,
-                                     void* workspace, size_t workspace_bytes, void* stream);
+                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -32,7 +32,7 @@ extern "C" {
 /* out and (when not NULL) lse = logsumexp of the logits; the errors of dsa3d_forward, with
  * logits taking the place of q and k (4-byte aligned). */
 dsa3d_status dsa3d_pw_forward(const dsa3d_desc* desc, const float* logits, const void* v,
-                              const float* offsets, void* out, float* lse, void* stream);
+                              const float* offsets, void* out, float* lse, hipStream_t stream);
 
 /* Workspace bytes dsa3d_pw_backward needs (the same binning as dsa3d_backward: about 56 bytes
  * per (row, point) and 12 per cell); 0 for a descriptor it would reject. */
@@ -50,7 +50,7 @@ size_t dsa3d_pw_backward_workspace_size(const dsa3d_desc* desc);
 dsa3d_status dsa3d_pw_backward(const dsa3d_desc* desc, const float* logits, const void* v,
                                const float* offsets, const float* lse, const void* dout,
                                float* dlogits, float* dv, float* d_offsets, void* workspace,
-                               size_t workspace_bytes, void* stream, void* const* events);
+                               size_t workspace_bytes, hipStream_t stream, const hipEvent_t* events);
 
 #ifdef __cplusplus
 }

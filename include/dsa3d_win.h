@@ -64,7 +64,7 @@ typedef struct {
  * DSA3D_ERR_ALIAS. */
 dsa3d_status dsa3d_win_forward(const dsa3d_win_desc* desc, const void* q, const void* k,
                                const void* v, void* out, void* out_res, float* lse,
-                               void* stream);
+                               hipStream_t stream);
 
 /* Workspace bytes dsa3d_win_backward needs: 4 per query row (Delta = <dout, out>), rounded up
  * to 256; 0 for a descriptor it would reject. */
@@ -95,8 +95,8 @@ size_t dsa3d_win_backward_workspace_size(const dsa3d_win_desc* desc);
 dsa3d_status dsa3d_win_backward(const dsa3d_win_desc* desc, const void* q, const void* k,
                                 const void* v, const void* out, const void* out_res,
                                 const float* lse, const void* dout, float* dq, float* dk, float* dv,
-                                void* workspace, size_t workspace_bytes, void* stream,
-                                void* const* events);
+                                void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                const hipEvent_t* events);
 
 #ifdef __cplusplus
 }

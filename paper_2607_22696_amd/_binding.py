@@ -19,8 +19,8 @@ DSA3D_ERR_INVALID_SHAPE = 2
 DSA3D_ERR_UNSUPPORTED = 3
 DSA3D_ERR_MISALIGNED = 4
 DSA3D_ERR_WORKSPACE = 5
-DSA3D_ERR_ALIAS = 6
-DSA3D_ERR_DEVICE = 7
+DSA3D_ERR_DEVICE = 6
+DSA3D_ERR_ALIAS = 7
 
 DSA3D_F32 = 0
 DSA3D_BF16 = 1
@@ -82,10 +82,10 @@ def load():
         vp, pd = ctypes.c_void_p, ctypes.POINTER(dsa3d_desc)
         lib.dsa3d_forward.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp]
         lib.dsa3d_forward.restype = ctypes.c_int
-        lib.dsa3d_backward.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+        lib.dsa3d_backward.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ctypes.c_size_t, vp]
         lib.dsa3d_backward.restype = ctypes.c_int
-        lib.dsa3d_backward_timed.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+        lib.dsa3d_backward_timed.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                              ctypes.c_size_t, vp, ctypes.POINTER(vp)]
         lib.dsa3d_backward_timed.restype = ctypes.c_int
         lib.dsa3d_pw_forward.argtypes = [pd, vp, vp, vp, vp, vp, vp]
@@ -164,26 +164,27 @@ def dsa3d_forward(desc, q, k, v, offsets, out, lse=None, stream=None, check=True
     return st
 
 
-def dsa3d_backward(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets,
+def dsa3d_backward(desc, q, k, v, offsets, out, lse, dout, dq, dk, dv, d_offsets,
                    workspace=None, workspace_bytes=0, stream=None, check=True) -> int:
+    """`out` (the forward's output) may be None: the library does not read it."""
     st = load().dsa3d_backward(ctypes.byref(desc) if desc is not None else None, _ptr(q), _ptr(k),
-                               _ptr(v), _ptr(offsets), _ptr(lse), _ptr(dout), _ptr(dq),
-                               _ptr(dk), _ptr(dv), _ptr(d_offsets), _ptr(workspace),
+                               _ptr(v), _ptr(offsets), _ptr(out), _ptr(lse), _ptr(dout),
+                               _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_offsets), _ptr(workspace),
                                workspace_bytes, _stream(stream))
     if check and st != DSA3D_OK:
         raise Dsa3dError(st, "dsa3d_backward")
     return st
 
 
-def dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets,
+def dsa3d_backward_timed(desc, q, k, v, offsets, out, lse, dout, dq, dk, dv, d_offsets,
                          workspace=None, workspace_bytes=0, stream=None, events=None,
                          check=True) -> int:
     """`events`: None or DSA3D_BACKWARD_PHASES + 1 torch.cuda.Event objects (or raw hipEvent_t
     addresses); each must already be created, i.e. recorded once."""
     arr = _event_array(events)
     st = load().dsa3d_backward_timed(ctypes.byref(desc) if desc is not None else None, _ptr(q),
-                                     _ptr(k), _ptr(v), _ptr(offsets), _ptr(lse), _ptr(dout),
-                                     _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_offsets),
+                                     _ptr(k), _ptr(v), _ptr(offsets), _ptr(out), _ptr(lse),
+                                     _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_offsets),
                                      _ptr(workspace), workspace_bytes, _stream(stream), arr)
     if check and st != DSA3D_OK:
         raise Dsa3dError(st, "dsa3d_backward_timed")

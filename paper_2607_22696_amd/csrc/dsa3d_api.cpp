@@ -101,7 +101,7 @@ const char* dsa3d_status_string(dsa3d_status s) {
 }
 
 dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
-                           const float* offsets, void* out, float* lse, void* stream) {
+                           const float* offsets, void* out, float* lse, hipStream_t stream) {
   dsa3d::Geometry g;
   uint64_t rows, io_bytes, f32_bytes, off_bytes;
   dsa3d_status st = check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes);
@@ -122,7 +122,7 @@ dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k,
       if (overlaps(sl, s)) return DSA3D_ERR_ALIAS;
   }
   const hipError_t e = dsa3d::launch_forward(g, desc->dtype == DSA3D_BF16, q, k, v, nullptr,
-                                             offsets, out, lse, static_cast<hipStream_t>(stream));
+                                             offsets, out, lse, stream);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
@@ -143,10 +143,11 @@ size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc) {
 }
 
 dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const void* k,
-                                  const void* v, const float* offsets, const float* lse,
-                                  const void* dout, float* dq, float* dk, float* dv,
-                                  float* d_offsets, void* workspace, size_t workspace_bytes,
-                                  void* stream, void* const* events) {
+                                  const void* v, const float* offsets, const void* out,
+                                  const float* lse, const void* dout, float* dq, float* dk,
+                                  float* dv, float* d_offsets, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream,
+                                  const hipEvent_t* events) {
   dsa3d::Geometry g;
   uint64_t rows, io_bytes, f32_bytes, off_bytes;
   dsa3d_status st = check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes);
@@ -159,12 +160,14 @@ dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const v
   if (workspace == nullptr || workspace_bytes < ws_need) return DSA3D_ERR_WORKSPACE;
   if (!aligned(workspace, 256)) return DSA3D_ERR_MISALIGNED;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dout, 16) ||
-      !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) ||
+      !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) || (out && !aligned(out, 16)) ||
       !aligned(offsets, 4) || !aligned(lse, 4) || !aligned(d_offsets, 4))
     return DSA3D_ERR_MISALIGNED;
+  // out (optional, not read) counts as an input: outputs and the workspace must avoid it
   const Span in[] = {span_of(q, io_bytes),         span_of(k, io_bytes),
                      span_of(v, io_bytes),         span_of(offsets, off_bytes),
-                     span_of(lse, rows * 4),       span_of(dout, io_bytes)};
+                     span_of(lse, rows * 4),       span_of(dout, io_bytes),
+                     span_of(out, out ? io_bytes : 0)};
   const Span outs[] = {span_of(dq, f32_bytes), span_of(dk, f32_bytes), span_of(dv, f32_bytes),
                        span_of(d_offsets, off_bytes)};
   const Span sw = span_of(workspace, ws_need);
@@ -177,19 +180,18 @@ dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const v
   }
   for (const Span& s : in)
     if (overlaps(sw, s)) return DSA3D_ERR_ALIAS;
-  const hipError_t e = dsa3d::launch_backward(
-      g, desc->dtype == DSA3D_BF16, q, k, v, nullptr, offsets, lse, dout, dq, dk, dv, d_offsets,
-      nullptr, workspace, static_cast<hipStream_t>(stream),
-      reinterpret_cast<hipEvent_t const*>(events));
+  const hipError_t e = dsa3d::launch_backward(g, desc->dtype == DSA3D_BF16, q, k, v, nullptr,
+                                              offsets, lse, dout, dq, dk, dv, d_offsets, nullptr,
+                                              workspace, stream, events);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
 dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
-                            const float* offsets, const float* lse, const void* dout, float* dq,
-                            float* dk, float* dv, float* d_offsets, void* workspace,
-                            size_t workspace_bytes, void* stream) {
-  return dsa3d_backward_timed(desc, q, k, v, offsets, lse, dout, dq, dk, dv, d_offsets, workspace,
-                              workspace_bytes, stream, nullptr);
+                            const float* offsets, const void* out, const float* lse,
+                            const void* dout, float* dq, float* dk, float* dv, float* d_offsets,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return dsa3d_backward_timed(desc, q, k, v, offsets, out, lse, dout, dq, dk, dv, d_offsets,
+                              workspace, workspace_bytes, stream, nullptr);
 }
 
 // ---------------------------------------------------------------------------- predicted weights
@@ -208,7 +210,7 @@ static dsa3d_status check_pw(const dsa3d_desc* desc, dsa3d::Geometry* g, uint64_
 }
 
 dsa3d_status dsa3d_pw_forward(const dsa3d_desc* desc, const float* logits, const void* v,
-                              const float* offsets, void* out, float* lse, void* stream) {
+                              const float* offsets, void* out, float* lse, hipStream_t stream) {
   dsa3d::Geometry g;
   uint64_t rows, io_bytes, f32_bytes, off_bytes, logit_bytes;
   dsa3d_status st = check_pw(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes, &logit_bytes);
@@ -230,7 +232,7 @@ dsa3d_status dsa3d_pw_forward(const dsa3d_desc* desc, const float* logits, const
   }
   // q and k are not read: v stands in for them so that every pointer the kernel forms is valid
   const hipError_t e = dsa3d::launch_forward(g, desc->dtype == DSA3D_BF16, v, v, v, logits,
-                                             offsets, out, lse, static_cast<hipStream_t>(stream));
+                                             offsets, out, lse, stream);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
@@ -246,7 +248,8 @@ size_t dsa3d_pw_backward_workspace_size(const dsa3d_desc* desc) {
 dsa3d_status dsa3d_pw_backward(const dsa3d_desc* desc, const float* logits, const void* v,
                                const float* offsets, const float* lse, const void* dout,
                                float* dlogits, float* dv, float* d_offsets, void* workspace,
-                               size_t workspace_bytes, void* stream, void* const* events) {
+                               size_t workspace_bytes, hipStream_t stream,
+                               const hipEvent_t* events) {
   dsa3d::Geometry g;
   uint64_t rows, io_bytes, f32_bytes, off_bytes, logit_bytes;
   dsa3d_status st = check_pw(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes, &logit_bytes);
@@ -279,8 +282,7 @@ dsa3d_status dsa3d_pw_backward(const dsa3d_desc* desc, const float* logits, cons
   // q, k, dq and dk are not used: valid pointers stand in for them
   const hipError_t e = dsa3d::launch_backward(
       g, desc->dtype == DSA3D_BF16, dout, v, v, logits, offsets, lse, dout, dv, dv, dv, d_offsets,
-      dlogits, workspace, static_cast<hipStream_t>(stream),
-      reinterpret_cast<hipEvent_t const*>(events));
+      dlogits, workspace, stream, events);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 

@@ -60,7 +60,7 @@ extern "C" {
 
 dsa3d_status dsa3d_dwconv3d_forward(const dsa3d_dwconv_desc* desc, const void* x,
                                     const float* weight, const float* bias, void* y,
-                                    int accumulate, void* stream) {
+                                    int accumulate, hipStream_t stream) {
   dsa3d::ConvGeometry g;
   uint64_t io_bytes, f32_bytes;
   const dsa3d_status st = check_conv(desc, &g, &io_bytes, &f32_bytes);
@@ -75,7 +75,7 @@ dsa3d_status dsa3d_dwconv3d_forward(const dsa3d_dwconv_desc* desc, const void* x
       (bias && overlaps(sy, span_of(bias, (uint64_t)g.C * 4))))
     return DSA3D_ERR_ALIAS;
   const hipError_t e = dsa3d::launch_conv_forward(g, desc->dtype == DSA3D_BF16, x, weight, bias, y,
-                                                  accumulate != 0, static_cast<hipStream_t>(stream));
+                                                  accumulate != 0, stream);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
@@ -89,7 +89,7 @@ size_t dsa3d_dwconv3d_backward_workspace_size(const dsa3d_dwconv_desc* desc) {
 dsa3d_status dsa3d_dwconv3d_backward(const dsa3d_dwconv_desc* desc, const void* x,
                                      const float* weight, const void* dy, float* dx,
                                      int accumulate_dx, float* dweight, float* dbias,
-                                     void* workspace, size_t workspace_bytes, void* stream) {
+                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
   dsa3d::ConvGeometry g;
   uint64_t io_bytes, f32_bytes;
   const dsa3d_status st = check_conv(desc, &g, &io_bytes, &f32_bytes);
@@ -120,7 +120,7 @@ dsa3d_status dsa3d_dwconv3d_backward(const dsa3d_dwconv_desc* desc, const void* 
   }
   const hipError_t e = dsa3d::launch_conv_backward(
       g, desc->dtype == DSA3D_BF16, x, weight, dy, dx, accumulate_dx != 0, dweight, dbias,
-      workspace, static_cast<hipStream_t>(stream));
+      workspace, stream);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 

@@ -61,7 +61,7 @@ extern "C" {
 
 dsa3d_status dsa3d_win_forward(const dsa3d_win_desc* desc, const void* q, const void* k,
                                const void* v, void* out, void* out_res, float* lse,
-                               void* stream) {
+                               hipStream_t stream) {
   dsa3d::WinGeometry g;
   uint64_t rows, io_bytes;
   const dsa3d_status st = check_win(desc, &g, &rows, &io_bytes);
@@ -80,7 +80,7 @@ dsa3d_status dsa3d_win_forward(const dsa3d_win_desc* desc, const void* q, const 
       if (overlaps(outs[a], outs[b])) return DSA3D_ERR_ALIAS;
   }
   const hipError_t e = dsa3d::launch_win_forward(g, q, k, v, out, out_res, lse,
-                                                 static_cast<hipStream_t>(stream));
+                                                 stream);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
@@ -94,8 +94,8 @@ size_t dsa3d_win_backward_workspace_size(const dsa3d_win_desc* desc) {
 dsa3d_status dsa3d_win_backward(const dsa3d_win_desc* desc, const void* q, const void* k,
                                 const void* v, const void* out, const void* out_res,
                                 const float* lse, const void* dout, float* dq, float* dk, float* dv,
-                                void* workspace, size_t workspace_bytes, void* stream,
-                                void* const* events) {
+                                void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                const hipEvent_t* events) {
   dsa3d::WinGeometry g;
   uint64_t rows, io_bytes;
   const dsa3d_status st = check_win(desc, &g, &rows, &io_bytes);
@@ -122,8 +122,8 @@ dsa3d_status dsa3d_win_backward(const dsa3d_win_desc* desc, const void* q, const
       if (overlaps(outs[a], outs[b])) return DSA3D_ERR_ALIAS;
   }
   const hipError_t e = dsa3d::launch_win_backward(
-      g, q, k, v, out, out_res, lse, dout, dq, dk, dv, workspace, static_cast<hipStream_t>(stream),
-      reinterpret_cast<hipEvent_t const*>(events));
+      g, q, k, v, out, out_res, lse, dout, dq, dk, dv, workspace, stream,
+      events);
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 

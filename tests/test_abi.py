@@ -58,8 +58,12 @@ def fwd(desc, **over):
                              args["lse"], stream=0, check=False)
 
 
+BWD_NAMES = ["q", "k", "v", "offsets", "out", "lse", "dout", "dq", "dk", "dv", "d_offsets",
+             "workspace"]
+
+
 def bwd(desc, **over):
-    names = ["q", "k", "v", "offsets", "lse", "dout", "dq", "dk", "dv", "d_offsets", "workspace"]
+    names = BWD_NAMES
     args = dict(zip(names, ptrs(len(names))))
     args["workspace_bytes"] = 1 << 33
     args.update(over)
@@ -129,9 +133,34 @@ def test_overlapping_outputs():
     assert fwd(d, out=q) == B.DSA3D_ERR_ALIAS
     assert fwd(d, out=q + 256) == B.DSA3D_ERR_ALIAS      # partial overlap of q's range
     assert fwd(d, lse=q + 1024) == B.DSA3D_ERR_ALIAS
-    names = ptrs(10)
-    assert bwd(d, dk=names[6]) == B.DSA3D_ERR_ALIAS      # dk == dq
+    names = ptrs(12)
+    assert bwd(d, dk=names[7]) == B.DSA3D_ERR_ALIAS      # dk == dq
     assert bwd(d, d_offsets=names[0] + 64) == B.DSA3D_ERR_ALIAS
+    assert bwd(d, dv=names[4] + 256) == B.DSA3D_ERR_ALIAS   # dv inside out
+
+
+def test_backward_out_is_optional_but_checked_when_given():
+    """out (the forward's output) is not read by the backward: NULL is accepted, a given
+    pointer must be aligned and must not overlap an output or the workspace."""
+    d = good_desc()
+    need = dsa.dsa3d_backward_workspace_size(d)
+    names = ptrs(12)
+    # NULL out passes the pointer checks: the call stops at the (later) workspace check
+    assert bwd(d, out=None, workspace_bytes=need - 1) == B.DSA3D_ERR_WORKSPACE
+    assert bwd(d, out=ptrs(16)[15] + 8) == B.DSA3D_ERR_MISALIGNED
+    assert bwd(d, out=names[7]) == B.DSA3D_ERR_ALIAS            # out == dq
+    assert bwd(d, out=names[11] + 1024) == B.DSA3D_ERR_ALIAS    # out inside the workspace
+    assert bwd_timed(d, out=names[8]) == B.DSA3D_ERR_ALIAS      # out == dk
+
+
+def test_status_codes_match_the_header():
+    src = open(os.path.join(INCLUDE, "dsa3d.h")).read()
+    codes = dict((n, int(v)) for n, v in re.findall(r"\b(DSA3D_(?:OK|ERR_[A-Z_]+))\s*=\s*(\d+)", src))
+    assert codes == {"DSA3D_OK": 0, "DSA3D_ERR_NULL_POINTER": 1, "DSA3D_ERR_INVALID_SHAPE": 2,
+                     "DSA3D_ERR_UNSUPPORTED": 3, "DSA3D_ERR_MISALIGNED": 4,
+                     "DSA3D_ERR_WORKSPACE": 5, "DSA3D_ERR_DEVICE": 6, "DSA3D_ERR_ALIAS": 7}
+    for n, v in codes.items():
+        assert getattr(B, n) == v, n
 
 
 def test_workspace_size_follows_the_documented_formula():
@@ -153,8 +182,8 @@ def test_workspace_errors():
     assert bwd(d, workspace=None) == B.DSA3D_ERR_WORKSPACE
     assert bwd(d, workspace_bytes=need - 1) == B.DSA3D_ERR_WORKSPACE
     assert bwd(d, workspace=ptrs(16)[15] + 128) == B.DSA3D_ERR_MISALIGNED
-    names = ptrs(11)
-    assert bwd(d, workspace=names[6]) == B.DSA3D_ERR_ALIAS          # workspace == dq
+    names = ptrs(12)
+    assert bwd(d, workspace=names[7]) == B.DSA3D_ERR_ALIAS          # workspace == dq
     assert bwd(d, workspace=names[0], workspace_bytes=need) == B.DSA3D_ERR_ALIAS  # == q
 
 
@@ -169,7 +198,7 @@ def test_backward_index_range_limit():
 
 
 def bwd_timed(desc, events=None, **over):
-    names = ["q", "k", "v", "offsets", "lse", "dout", "dq", "dk", "dv", "d_offsets", "workspace"]
+    names = BWD_NAMES
     args = dict(zip(names, ptrs(len(names))))
     args["workspace_bytes"] = 1 << 33
     args.update(over)
@@ -182,9 +211,10 @@ def bwd_timed(desc, events=None, **over):
 def test_timed_backward_validates_like_backward():
     d = good_desc()
     need = dsa.dsa3d_backward_workspace_size(d)
-    names = ptrs(11)
+    names = ptrs(12)
     cases = [dict(q=None), dict(d_offsets=None), dict(dq=ptrs(16)[15] + 4),
-             dict(workspace=None), dict(workspace_bytes=need - 1), dict(dk=names[6])]
+             dict(workspace=None), dict(workspace_bytes=need - 1), dict(dk=names[7]),
+             dict(out=names[9])]
     fake_events = list(range(1 << 12, (1 << 12) + B.DSA3D_BACKWARD_PHASES + 1))
     for over in cases:
         want = bwd(d, **over)
