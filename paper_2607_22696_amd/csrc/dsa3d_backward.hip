@@ -87,7 +87,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
     const float* __restrict__ logits, const float* __restrict__ offsets,
     const float* __restrict__ lse, const void* __restrict__ dout, float* __restrict__ dq,
     PointRec* __restrict__ recs, float* __restrict__ delta_out, uint32_t* __restrict__ counts,
-    int tiles) {
+    PencilOrder po) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -98,22 +98,22 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
   const char* kb = static_cast<const char*>(k);
   const char* vb = static_cast<const char*>(v);
   const char* gb = static_cast<const char*>(dout);
-  const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   const int HW = g.H * g.W;
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const int khw = g.kh * g.kw;
 
-  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
-       tile += gridDim.x) {
-    const int bh = tile / tiles_per_bh;
+  for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
+    PencilTile tl;
+    if (!pencil_tile(po, vt, tl)) continue;  // the whole block: no pencil left on this XCD
+    const int bh = tl.group;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int n0 = (tile % tiles_per_bh) * LY::kRowsPerBlock;
-    const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, n0 / HW);
-    const int n = n0 + wave * LY::kGroups + grp;
-    // All lanes of a group share n: a whole group is idle or active, so neither the group
-    // reductions nor the point sharing ever mix an idle group into an active one.
-    if (n >= g.N) continue;
-    const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
+    const int t = tl.frame;
+    const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, t);
+    int i, j;
+    // All lanes of a group share the token: a whole group is idle or active, so neither the
+    // group reductions nor the point sharing ever mix an idle group into an active one.
+    if (!pencil_cell(po, tl, wave * LY::kGroups + grp, i, j)) continue;
+    const int n = t * HW + i * g.W + j;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
     uint4 qr = make_uint4(0u, 0u, 0u, 0u);
@@ -468,27 +468,25 @@ template <int D, bool BF16, bool PW>
 __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_gather_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ dout,
     const uint32_t* __restrict__ starts, const Entry* __restrict__ entries, float* __restrict__ dk,
-    float* __restrict__ dv, int tiles) {
+    float* __restrict__ dv, PencilOrder po) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
-  const int Wb = (g.W + 1) / 2, Hb = (g.H + 1) / 2;  // blocks per grid row / column
-  const int Nb = g.T * Hb * Wb;
-  const int tiles_per_bh = (Nb + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   const uint32_t tok_bytes = (uint32_t)g.heads * LY::kRowBytes;  // one token's rows, all heads
 
-  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
-       tile += gridDim.x) {
-    const int bh = tile / tiles_per_bh;
+  for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
+    PencilTile tl;
+    if (!pencil_tile(po, vt, tl)) continue;
+    const int bh = tl.group;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int nb = (tile % tiles_per_bh) * LY::kRowsPerBlock + wave * LY::kGroups + grp;
-    if (nb >= Nb) continue;
+    int by, bx;  // the group's 2 x 2 block (cell of the pencil grid)
+    if (!pencil_cell(po, tl, wave * LY::kGroups + grp, by, bx)) continue;
     const int64_t head_off = ((int64_t)b * g.N * g.heads + m) * LY::kRowBytes + sub * 16;
     const char* qh = static_cast<const char*>(q) + head_off;
     const char* gh = static_cast<const char*>(dout) + head_off;
-    const int x0 = 2 * (nb % Wb), y0 = 2 * ((nb / Wb) % Hb), z = nb / (Wb * Hb);
+    const int x0 = 2 * bx, y0 = 2 * by, z = tl.frame;
     const bool hasx1 = x0 + 1 < g.W, hasy1 = y0 + 1 < g.H;
     BlockAcc<VEC> acc;
 #pragma unroll
@@ -670,7 +668,7 @@ template <int D, bool PW>
 __global__ __launch_bounds__(64 * gather_waves<D>()) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 3 : 2)))
 void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* __restrict__ dout,
                             const uint32_t* __restrict__ starts, const Entry* __restrict__ entries,
-                            float* __restrict__ dk, float* __restrict__ dv, int tiles) {
+                            float* __restrict__ dk, float* __restrict__ dv, PencilOrder po) {
   constexpr int NW = gather_waves<D>();
   constexpr int DB = D / 16;     // 16-channel blocks: two products each (hi, lo) per tensor
   constexpr int LPR = D / 8;     // lanes per row when copying rows (16 bytes each)
@@ -680,20 +678,18 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   GatherLds<D, PW>& L = lds[wave];
-  const int Xb = (g.W + 3) / 4, Yb = (g.H + 1) / 2, Zb = (g.T + 1) / 2;
-  const int nblk = Xb * Yb * Zb;  // voxel blocks per (b, head)
-  const int tiles_per_bh = (nblk + NW - 1) / NW;
   const uint32_t tok_bytes = (uint32_t)g.heads * 2 * D;
   const bool upper = lane >= 32;  // dV coefficients (else dK)
   const int own = lane & 31;      // the entry whose coefficients this lane forms
 
-  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
-       tile += gridDim.x) {
-    const int bh = tile / tiles_per_bh;
-    const int blk = (tile % tiles_per_bh) * NW + wave;
-    if (blk >= nblk) continue;
+  for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
+    PencilTile tl;
+    if (!pencil_tile(po, vt, tl)) continue;
+    int by, bx;  // the wave's 4 x 2 x 2 block: cell (by, bx) of the pencil grid, frame pair tl.frame
+    if (!pencil_cell(po, tl, wave, by, bx)) continue;
+    const int bh = tl.group;
     const int b = bh / g.heads, m = bh % g.heads;
-    const int x0 = 4 * (blk % Xb), y0 = 2 * ((blk / Xb) % Yb), z0 = 2 * (blk / (Xb * Yb));
+    const int x0 = 4 * bx, y0 = 2 * by, z0 = 2 * tl.frame;
     const int nx = min(5, g.W - x0 + 1);  // cells x0 - 1 .. x0 + nx - 2 exist
     const bool hasy1 = y0 + 1 < g.H, hasz1 = z0 + 1 < g.T;
     const int64_t head_off = ((int64_t)b * g.N * g.heads + m) * (2 * D) + (lane % LPR) * 16;
@@ -941,14 +937,14 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   }
-  const int tiles = tiles_for<D, BF16>(g);
-  const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
+  const PencilOrder po = query_order<D, BF16>(g);
+  const int blocks = grid_blocks(po.vtiles);
   if ((e = mark(0)) != hipSuccess) return e;
   {
     void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,       (void*)&v,
                  (void*)&logits, (void*)&off,  (void*)&lse,     (void*)&dout,
                  (void*)&dq,   (void*)&w.recs, (void*)&w.delta, (void*)&w.counts,
-                 (void*)&tiles};
+                 (void*)&po};
     const void* kern = pw ? reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, true>)
                           : reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, false>);
     e = hipLaunchKernel(kern, dim3(blocks), dim3(kBlockThreads), a, 0, s);
@@ -984,22 +980,24 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   if ((e = mark(3)) != hipSuccess) return e;
   if constexpr (BF16) {
     constexpr int NW = gather_waves<D>();
-    const int64_t vblocks = (int64_t)((g.T + 1) / 2) * ((g.H + 1) / 2) * ((g.W + 3) / 4);
-    const int gtiles = (int)((vblocks + NW - 1) / NW * g.B * g.heads);
-    const int gblocks = gtiles < kMaxBlocks ? gtiles : kMaxBlocks;
+    // cells: 4 x 2 voxel blocks of a frame pair; pencils of about 16 x 16 voxels
+    const PencilOrder go = plan_pencils(g.B * g.heads, (g.T + 1) / 2, (g.H + 1) / 2,
+                                        (g.W + 3) / 4, NW, 8, 4);
+    const int gblocks = grid_blocks(go.vtiles);
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
-                 (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&gtiles};
+                 (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&go};
     const void* kern = pw ? reinterpret_cast<const void*>(&bwd_gather_mfma_kernel<D, true>)
                           : reinterpret_cast<const void*>(&bwd_gather_mfma_kernel<D, false>);
     e = hipLaunchKernel(kern, dim3(gblocks), dim3(64 * NW), a, 0, s);
     if (e != hipSuccess) return e;
   } else {
     using LY = Layout<D, BF16>;
-    const int64_t vblocks = (int64_t)g.T * ((g.H + 1) / 2) * ((g.W + 1) / 2);
-    const int gtiles = (int)((vblocks + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock * g.B * g.heads);
-    const int gblocks = gtiles < kMaxBlocks ? gtiles : kMaxBlocks;
+    // cells: 2 x 2 voxel blocks of a frame; pencils of about 16 x 16 voxels
+    const PencilOrder go = plan_pencils(g.B * g.heads, g.T, (g.H + 1) / 2, (g.W + 1) / 2,
+                                        LY::kRowsPerBlock, 8, 8);
+    const int gblocks = grid_blocks(go.vtiles);
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
-                 (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&gtiles};
+                 (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&go};
     const void* kern = pw ? reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16, true>)
                           : reinterpret_cast<const void*>(&bwd_gather_kernel<D, BF16, false>);
     e = hipLaunchKernel(kern, dim3(gblocks), dim3(kBlockThreads), a, 0, s);

@@ -11,6 +11,9 @@
 
 #include "dsa3d_internal.h"
 
+#define DSA3D_TILE_FN __host__ __device__ inline __attribute__((always_inline))
+#include "tile_order.h"
+
 namespace dsa3d {
 namespace dev {
 
@@ -126,31 +129,6 @@ __device__ inline __attribute__((always_inline)) int xcd_tile(int bid, int nbloc
   const int xcd = bid % kNumXcd, slot = bid / kNumXcd;
   const int per = nblocks / kNumXcd, rem = nblocks % kNumXcd;
   return xcd * per + min(xcd, rem) + slot;
-}
-
-// Tiles per XCD chunk of xcd_window_tile, measured on one MI355X: at head_dim 64 (32-token
-// tiles) 256 tiles ran the 64x34x60 forward + backward in 15.2-15.4 ms against 15.5-15.7 for
-// 16-128 and 16.0-16.3 for the one-range-per-XCD order; at head_dim 128 (16-token tiles) 64
-// tiles ran the 256x68x120 forward in 206-207 ms against 211-224 for 32, 128, 256 and 512,
-// 293 for 16 and 243-244 for the one-range order.
-template <int D>
-constexpr int xcd_chunk() {
-  return D >= 128 ? 64 : 256;
-}
-
-// Logical tile of a block for the query- and voxel-owned 3D-DSA kernels.  Blocks reach the
-// XCDs round-robin (block b runs on XCD b % 8), so tiles are handed out in windows of
-// 8 * CHUNK: inside a window XCD x takes the CHUNK consecutive tiles that start at
-// x * CHUNK.  Each XCD's L2 then serves a contiguous run of tiles, and the eight XCDs work
-// on neighbouring runs of one head at a time, whose K/V rows share the memory-side cache
-// (with one contiguous range per XCD, the XCDs work on eight different heads at once).
-// Blocks past the last whole window keep their own index.
-template <int CHUNK>
-__device__ inline __attribute__((always_inline)) int xcd_window_tile(int bid, int nblocks) {
-  constexpr int kWin = kNumXcd * CHUNK;
-  if (bid >= nblocks / kWin * kWin) return bid;
-  const int xcd = bid % kNumXcd, slot = bid / kNumXcd;
-  return slot / CHUNK * kWin + xcd * CHUNK + slot % CHUNK;
 }
 
 // ---------------------------------------------------------------------------- corner rows
@@ -312,11 +290,17 @@ __device__ inline __attribute__((always_inline)) void load_shared_corners(
 
 constexpr int kMaxBlocks = 1 << 22;  // grid cap; larger problems loop over tiles
 
-template <int D, bool BF16, int NC = 1>
-inline int tiles_for(const Geometry& g) {
-  using LY = Layout<D, BF16, NC>;
-  const int64_t per = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
-  return (int)(per * g.B * g.heads);
+// Pencil order of the query-owned kernels: tiles of kRowsPerBlock tokens inside pencils of
+// about 16 x 16 tokens of a frame.
+template <int D, bool BF16>
+inline PencilOrder query_order(const Geometry& g) {
+  return plan_pencils(g.B * g.heads, g.T, g.H, g.W, Layout<D, BF16>::kRowsPerBlock, 16, 16);
+}
+
+// Workgroups for `vtiles` virtual tiles: at most kMaxBlocks, a multiple of 8 when capped so
+// that a workgroup's later tiles (v += gridDim.x) stay on its XCD.
+inline int grid_blocks(int64_t vtiles) {
+  return (int)(vtiles < kMaxBlocks ? vtiles : kMaxBlocks);
 }
 
 }  // namespace dev

@@ -10,10 +10,9 @@
 // corner row is read once.  Nothing per point is written to memory; the output row and
 // its LSE are stored once.
 //
-// Memory order: consecutive workgroups go to the 8 XCDs round-robin; blocks are renumbered
-// so that each XCD walks contiguous runs of (batch, head, token) tiles while the eight XCDs
-// work on neighbouring runs of one head, sharing that head's band of K/V rows in the
-// memory-side cache.
+// Memory order: tiles are handed out in pencils (tile_order.h): each XCD walks one pencil of
+// about 16 x 16 tokens of a (batch, head) frame by frame, so the K/V rows its in-flight
+// queries reach stay in its L2.
 #include "dsa3d_device.h"
 
 namespace dsa3d {
@@ -32,7 +31,7 @@ template <int D, bool BF16, bool PW>
 __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
     const float* __restrict__ logits, const float* __restrict__ offsets, void* __restrict__ out,
-    float* __restrict__ lse, int tiles) {
+    float* __restrict__ lse, PencilOrder po) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -42,21 +41,23 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
   const char* qb = static_cast<const char*>(q);
   const char* kb = static_cast<const char*>(k);
   const char* vb = static_cast<const char*>(v);
-  const int tiles_per_bh = (g.N + LY::kRowsPerBlock - 1) / LY::kRowsPerBlock;
   const int HW = g.H * g.W;
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const int khw = g.kh * g.kw;
 
-  for (int tile = xcd_window_tile<xcd_chunk<D>()>(blockIdx.x, gridDim.x); tile < tiles;
-       tile += gridDim.x) {
-    const int bh = tile / tiles_per_bh;
-    const int b = bh / g.heads, m = bh % g.heads;
-    const int n0 = (tile % tiles_per_bh) * LY::kRowsPerBlock;
-    const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, n0 / HW);
-    const int n_raw = n0 + wave * LY::kGroups + grp;
-    const bool active = n_raw < g.N;
-    const int n = active ? n_raw : g.N - 1;
-    const int j = n % g.W, i = (n / g.W) % g.H, t = n / HW;
+  for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
+    PencilTile tl;
+    if (!pencil_tile(po, vt, tl)) continue;  // the whole block: no pencil left on this XCD
+    const int b = tl.group / g.heads, m = tl.group % g.heads;
+    const int t = tl.frame;
+    const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, t);
+    int i, j;
+    const bool active = pencil_cell(po, tl, wave * LY::kGroups + grp, i, j);
+    if (!active) {  // an idle row computes on a valid token and stores nothing
+      i = tl.pr * po.ph;
+      j = tl.pc * po.pw;
+    }
+    const int n = t * HW + i * g.W + j;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
     uint4 qr = make_uint4(0u, 0u, 0u, 0u);
@@ -102,9 +103,12 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
         }
         // One exponential per point: a new maximum rescales the running sums by
         // 2^(old max - new max) and enters with weight exactly 1; otherwise the point enters
-        // with 2^(s - max).  (The first point always takes the first branch: 2^-inf = 0.)
+        // with 2^(s - max).  (A first finite logit takes the first branch: 2^-inf = 0.)  A
+        // given logit of -inf enters with weight 0 even while the maximum is still -inf,
+        // where s - max would be NaN.
         const bool up = s2 > mx;
-        const float ex = exp2f(up ? mx - s2 : s2 - mx);
+        float ex = exp2f(up ? mx - s2 : s2 - mx);
+        if constexpr (PW) ex = s2 == -INFINITY ? 0.0f : ex;
         const float corr = up ? ex : 1.0f;
         const float e = up ? 1.0f : ex;
         l = fmaf(l, corr, e);
@@ -139,10 +143,10 @@ template <int D, bool BF16>
 hipError_t fwd_dispatch(const Geometry& g, const void* q, const void* k, const void* v,
                         const float* logits, const float* off, void* out, float* lse,
                         hipStream_t s) {
-  const int tiles = tiles_for<D, BF16>(g);
-  const int blocks = tiles < kMaxBlocks ? tiles : kMaxBlocks;
+  const PencilOrder po = query_order<D, BF16>(g);
+  const int blocks = grid_blocks(po.vtiles);
   void* args[] = {(void*)&g,   (void*)&q,   (void*)&k,   (void*)&v,    (void*)&logits,
-                  (void*)&off, (void*)&out, (void*)&lse, (void*)&tiles};
+                  (void*)&off, (void*)&out, (void*)&lse, (void*)&po};
   const void* kern = logits != nullptr ? reinterpret_cast<const void*>(&fwd_kernel<D, BF16, true>)
                                        : reinterpret_cast<const void*>(&fwd_kernel<D, BF16, false>);
   return hipLaunchKernel(kern, dim3(blocks), dim3(kBlockThreads), args, 0, s);

@@ -132,3 +132,26 @@ def test_pw_64x34x60_full_size():
         check(f"dv[frame {f}, head {m}]", to_host(dv[0, f, :, :, m]), rdv[f], True)
         check(f"dlogits[frames {t0}-{t1}, head {m}]", to_host(dl[0, t0:t1, :, :, m]), rdl, True)
         check(f"d_offsets[frames {t0}-{t1}, head {m}]", to_host(doff[0, t0:t1, :, :, m]), rdo, True)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_minus_infinity_logits(dtype):
+    """Logits of -inf drop their points (weight 0): the leading 1 to 3 points of every row
+    and one point in the middle, so a row's first logits are -inf while its running maximum
+    is still -inf."""
+    w = small(f"pw_neginf_{dtype}", T=3, H=6, W=7, heads=2, head_dim=64, dtype=dtype, seed=45)
+    bf = dtype == "bf16"
+    logits, v, off, dout = testgen.gen_pw_inputs(w)
+    lead = 1 + np.arange(logits[..., 0].size).reshape(logits.shape[:-1]) % 3
+    for p in range(3):
+        logits[..., p][lead > p] = -np.inf
+    logits[..., 13] = -np.inf
+    out, lse, dl, dv, doff = run(w, (logits, v, off, dout))
+    ro, rl = oracle.pw_forward(shape9(w), w.dtype, logits, v, off)
+    rdl, rdv, rdo = oracle.pw_backward(shape9(w), w.dtype, logits, v, off, dout)
+    assert np.all(np.isfinite(ro)) and np.all(np.isfinite(to_host(out)))
+    check("out", to_host(out).reshape(ro.shape), ro, bf)
+    check("lse", to_host(lse).reshape(-1), rl, bf)
+    check("dlogits", to_host(dl), rdl, bf)
+    check("dv", to_host(dv), rdv, bf)
+    check("d_offsets", to_host(doff), rdo, bf)

@@ -137,3 +137,25 @@ def test_bf16_values_are_read_exactly():
     np.testing.assert_array_equal(a[2], b[2])   # d_offsets
     # dV is scattered by OpenMP threads with atomic adds: only the summation order may differ
     np.testing.assert_allclose(a[1], b[1], rtol=0, atol=1e-12)
+
+
+def test_minus_infinity_logits_drop_their_points():
+    """A logit of -inf takes its point out of the softmax (weight exactly 0), here for the
+    leading points of every row (1 to 3 of them) and for one point in the middle; the
+    result is the grid_sample route's, whose softmax gives those points weight 0."""
+    B, T, H, W, M, D, kt, kh, kw = 1, 3, 4, 5, 2, 8, 3, 3, 3
+    shape = (B, T, H, W, M, D, kt, kh, kw)
+    v, logits, off, dout = case(6, B, T, H, W, M, D, kt, kh, kw)
+    lead = 1 + np.arange(B * T * H * W * M).reshape(B, T, H, W, M) % 3
+    for p in range(3):
+        logits[..., p][lead > p] = -np.inf
+    logits[..., 13] = -np.inf
+    ro, rl, rdl, rdv, rdo = torch_route(v, logits, off, kt, kh, kw, dout)
+    out, lse = oracle.pw_forward(shape, "f32", logits, v, off)
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse))
+    np.testing.assert_allclose(out.reshape(ro.shape), ro, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse.reshape(rl.shape), rl, rtol=0, atol=1e-12)
+    dl, dv, do = oracle.pw_backward(shape, "f32", logits, v, off, dout)
+    np.testing.assert_allclose(dl, rdl, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dv, rdv, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(do, rdo, rtol=0, atol=1e-10)
