@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 METRIC = "3D-DSA fwd+bwd queries/s and achieved HBM GB/s (% of peak) at 1 GPU"
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 VALU_PEAK_TFLOPS = 157.3        # MI355X fp32 vector peak (2 FLOP/lane/clk: dot2 / dual issue)
-DEFAULT_WORKLOAD = "fwdbwd_64x34x60"
+DEFAULT_WORKLOAD = "wide_64x68x120_p75"
 DEFAULT_CONV_WORKLOAD = "dwconv_1080p_256f"
 DEFAULT_PW_WORKLOAD = "pw_64x34x60"
 PW_METRIC = "3D-DSA predicted-weights fwd+bwd queries/s and achieved HBM GB/s (% of peak) at 1 GPU"
@@ -41,7 +41,7 @@ CSRC = os.path.join(ROOT, "paper_2607_22696_amd", "csrc")
 
 # Device sources of each kernel family: counter figures taken from other sources are stale.
 FAMILY_SOURCES = {
-    "dsa": ["dsa3d_device.h", "dsa3d_forward.hip", "dsa3d_backward.hip"],
+    "dsa": ["dsa3d_device.h", "tile_order.h", "dsa3d_forward.hip", "dsa3d_backward.hip"],
     "dwconv": ["dsa3d_device.h", "dwconv3d.hip"],
     "win": ["winattn.hip"],
 }
@@ -73,37 +73,69 @@ def kernel_base(name: str) -> str:
     return "bwd_gather_kernel" if base == "bwd_gather_mfma_kernel" else base
 
 
-def pmc_summary(workload, fetch_dir, write_dir, copyf_dir, copyw_dir, copy_mib):
-    """Turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE of the bench command, and of
-    a device copy of copy_mib MiB) into profiles/traffic_<workload>.json: HBM bytes per
-    launch of each kernel, each counter scaled by what it reads for the copy of known size."""
+# Counters of the two rocprofv3 --pmc passes that give a kernel's traffic past the L2s
+# (each pass within the 4 TCC counters one run can hold):
+READ_COUNTERS = ("TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum", "TCC_EA0_RDREQ_128B_sum",
+                 "TCC_EA0_RDREQ_sum")
+WRITE_COUNTERS = ("WRITE_SIZE", "TCC_ATOMIC_sum", "TCC_EA0_ATOMIC_sum")
+
+
+def pmc_summary(workload, read_dir, write_dir, copyr_dir, copyw_dir, copy_mib):
+    """Turn four rocprofv3 --pmc runs (READ_COUNTERS and WRITE_COUNTERS of the bench command,
+    and of a device copy of copy_mib MiB) into profiles/traffic_<workload>.json: per launch of
+    each kernel, the bytes read past the L2s (read requests to the memory side times their
+    size: 32, 64 or 128 bytes), the bytes written (WRITE_SIZE), and the atomic requests at the
+    L2s (TCC_ATOMIC) and past them (TCC_EA0_ATOMIC).  The copy checks the accounting: its read
+    and write bytes per byte copied are stored beside the kernels' figures.  (The derived
+    FETCH_SIZE counter counts 64 bytes per 128-byte read request on this GPU, half the bytes,
+    which is why the request counters are read directly.)"""
     import csv
 
     def per_kernel(d):
         path = [os.path.join(d, f) for f in os.listdir(d) if f.endswith("counter_collection.csv")][0]
         acc = {}
         for r in csv.DictReader(open(path)):
-            acc.setdefault(kernel_base(r["Kernel_Name"]), []).append(
-                float(r["Counter_Value"]) * 1024.0)  # KiB -> B
-        return acc
+            key = (kernel_base(r["Kernel_Name"]), r["Dispatch_Id"])
+            acc.setdefault(key, {})[r["Counter_Name"]] = float(r["Counter_Value"])
+        out = {}
+        for (k, _), c in acc.items():
+            out.setdefault(k, []).append(c)
+        return out
 
-    fetch, write = per_kernel(fetch_dir), per_kernel(write_dir)
+    def read_bytes(c):
+        return (32 * c["TCC_EA0_RDREQ_32B_sum"] + 64 * c["TCC_EA0_RDREQ_64B_sum"]
+                + 128 * c["TCC_EA0_RDREQ_128B_sum"])
+
+    def mean(xs):
+        return sum(xs) / len(xs)
+
+    reads, writes = per_kernel(read_dir), per_kernel(write_dir)
     true_bytes = copy_mib * (1 << 20)
-    cf = per_kernel(copyf_dir)["__amd_rocclr_copyBuffer"]
+    cr = per_kernel(copyr_dir)["__amd_rocclr_copyBuffer"]
     cw = per_kernel(copyw_dir)["__amd_rocclr_copyBuffer"]
-    fetch_scale = (sum(cf) / len(cf)) / true_bytes   # counter bytes per byte actually read
-    write_scale = (sum(cw) / len(cw)) / true_bytes
     out = {"workload": workload, "kernel_source_hash": kernel_source_hash(workload_family(workload)),
-           "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
+           "counted_at": "past the L2s: read requests x size (TCC_EA0_RDREQ_32B/64B/128B), "
+                         "WRITE_SIZE; memory-side-cache hits count too",
+           "copy_check": {"mib": copy_mib,
+                          "read_bytes_per_byte": round(mean([read_bytes(c) for c in cr]) / true_bytes, 4),
+                          "write_bytes_per_byte": round(mean([c["WRITE_SIZE"] * 1024.0 for c in cw])
+                                                        / true_bytes, 4)},
            "kernels": {}}
-    for k in fetch:
+    for k in reads:
         # the operator's kernels only (not the copy, fills or the gather microbenchmark)
-        if k not in write or not k.endswith("_kernel"):
+        if k not in writes or not k.endswith("_kernel"):
             continue
-        f = sum(fetch[k]) / len(fetch[k]) / fetch_scale
-        w = sum(write[k]) / len(write[k]) / write_scale
-        out["kernels"][k] = {"fetch_bytes": round(f), "write_bytes": round(w),
-                             "hbm_bytes": round(f + w)}
+        rd = mean([read_bytes(c) for c in reads[k]])
+        req = mean([c["TCC_EA0_RDREQ_sum"] for c in reads[k]])
+        sized = mean([c["TCC_EA0_RDREQ_32B_sum"] + c["TCC_EA0_RDREQ_64B_sum"]
+                      + c["TCC_EA0_RDREQ_128B_sum"] for c in reads[k]])
+        wr = mean([c["WRITE_SIZE"] * 1024.0 for c in writes[k]])
+        out["kernels"][k] = {"fetch_bytes": round(rd), "write_bytes": round(wr),
+                             "hbm_bytes": round(rd + wr),
+                             "read_requests_of_known_size": round(sized / max(req, 1.0), 4),
+                             "atomics_l2": round(mean([c["TCC_ATOMIC_sum"] for c in writes[k]])),
+                             "atomics_past_l2": round(mean([c["TCC_EA0_ATOMIC_sum"]
+                                                            for c in writes[k]]))}
     os.makedirs(PROFILES, exist_ok=True)
     path = os.path.join(PROFILES, f"traffic_{workload}.json")
     with open(path, "w") as fh:
@@ -125,9 +157,13 @@ def measured_traffic(workload, kernel):
     return None if k is None else k["hbm_bytes"]
 
 
-# kernels of one backward call, in launch order (the bin scan is four small kernels)
-BWD_KERNELS = ("bwd_sweep_kernel", "fill_u32_kernel", "scan_reduce_kernel", "scan_sums_kernel",
-               "scan_apply_kernel", "bwd_finalize_kernel", "bwd_gather_kernel")
+# kernels of one backward call of the main operator, in launch order (the bin scan is three
+# small kernels after the fill of the counts)
+BWD_KERNELS = ("fill_u32_kernel", "bwd_vpass_kernel", "scan_reduce_kernel", "scan_sums_kernel",
+               "scan_apply_kernel", "bwd_kpass_kernel", "bwd_gather_kernel")
+# the backward's four timed phases (dsa3d_backward_timed), main operator and predicted weights
+BWD_PHASES = ("bwd_vpass_kernel", "bin_scan", "bwd_kpass_kernel", "bwd_gather_kernel")
+PW_BWD_PHASES = ("bwd_sweep_kernel", "bin_scan", "bwd_finalize_kernel", "bwd_gather_kernel")
 
 
 def measured_step_traffic(workload, backward):
@@ -144,15 +180,59 @@ def measured_step_traffic(workload, backward):
     return total
 
 
-def hbm_rocprof(workload, backward, ms_step):
-    """The step's HBM traffic as rocprofv3 counted it (FETCH_SIZE + WRITE_SIZE, calibrated on
-    a device copy) over the step time measured in this run: GB/s and fraction of the 8 TB/s
-    peak, or None where no counters for the current kernel sources are committed."""
+def hbm_rocprof(workload, backward, ms_step, alg_bytes):
+    """The step's traffic past the L2s as rocprofv3 counted it (read requests x size plus
+    WRITE_SIZE, profiles/traffic_<workload>.json) over the step time measured in this run:
+    GB/s, fraction of the 8 TB/s HBM peak, and the ratio to the step's algorithmic bytes (what
+    the counters see beyond the compulsory traffic: re-reads of corner rows that missed L2,
+    workspace, atomics).  Rows served by the memory-side cache count too, so this is an upper
+    bound on DRAM traffic.  None where no counters for the current kernel sources are
+    committed."""
     b = measured_step_traffic(workload, backward)
     if b is None:
         return None
     gbs = b / (ms_step * 1e-3) / 1e9
-    return {"bytes_per_step": b, "GBps": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    return {"counted_at": "L2 egress", "bytes_per_step": b, "GBps": round(gbs, 1),
+            "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "ratio_to_algorithmic": round(b / alg_bytes, 2)}
+
+
+def copy_ceiling(torch, mib=2048):
+    """A device-to-device copy of `mib` MiB on the bench's device: read + write GB/s, the
+    practical ceiling of HBM traffic on this machine."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    t = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t[0].record()
+    for _ in range(5):
+        dst.copy_(src)
+    t[1].record()
+    torch.cuda.synchronize()
+    ms = t[0].elapsed_time(t[1]) / 5
+    gbs = 2 * n * 4 / (ms * 1e-3) / 1e9
+    del src, dst
+    return {"what": f"device-to-device copy of {mib} MiB, read + write bytes",
+            "GBps": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def host_info():
+    """CPU model, logical CPUs and RAM of the machine the oracle runs on."""
+    model, ram = "unknown", None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal"):
+                ram = round(int(line.split()[1]) / (1 << 20), 1)
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "ram_GiB": ram}
 
 
 def algorithmic(w):
@@ -161,10 +241,12 @@ def algorithmic(w):
     Per query row (token, head), with s = bytes per q/k/v element, P points, head_dim D:
       fwd_kernel           bytes  q, k, v read + out written (4 D s), offsets (12 P), lse (4)
                            flops  16 P D multiply-adds: 8 corners x D for q.K, 8 x D for V
-      bwd_sweep_kernel     bytes  q, k, v, dout read (4 D s), offsets (12 P), lse (4), dq (4 D)
-                           flops  24 P D multiply-adds: q.K_c and dout.V_c at 8 corners, and
-                                  the 8-corner K interpolation that dq needs
-      bwd_finalize_kernel  bytes  offsets read (12 P), d_offsets written (12 P)
+      bwd_vpass_kernel     bytes  v, dout read (2 D s), offsets (12 P)
+                           flops  8 P D multiply-adds: dout.V_c at 8 corners
+      bwd_kpass_kernel     bytes  q, k read (2 D s), offsets (12 P), lse (4), dq and
+                                  d_offsets written (4 D + 12 P)
+                           flops  16 P D multiply-adds: q.K_c at 8 corners and the 8-corner
+                                  K interpolation that dq needs
       bwd_gather_kernel    bytes  q, dout read (2 D s), dk, dv written (8 D)
                            flops  16 P D multiply-adds: w_c ds_p q into dK and w_c alpha_p dout
                                   into dV at 8 corners
@@ -178,8 +260,8 @@ def algorithmic(w):
     P, D = w.P, w.head_dim
     per = {
         "fwd_kernel": (4 * D * s + 12 * P + 4, 32 * P * D),
-        "bwd_sweep_kernel": (4 * D * s + 12 * P + 4 + 4 * D, 48 * P * D),
-        "bwd_finalize_kernel": (24 * P, 0),
+        "bwd_vpass_kernel": (2 * D * s + 12 * P, 16 * P * D),
+        "bwd_kpass_kernel": (2 * D * s + 12 * P + 4 + 4 * D + 12 * P, 32 * P * D),
         "bwd_gather_kernel": (2 * D * s + 8 * D, 32 * P * D),
         "forward": (4 * D * s + 12 * P + 4, 32 * P * D),
         "backward": (4 * D * s + 12 * P + 4 + 3 * D * 4 + 12 * P, 80 * P * D),
@@ -191,42 +273,86 @@ def vmem_bytes(w):
     """Bytes that the vector-memory instructions (loads and stores through each compute
     unit's L1 path) of the query-owned kernels move per launch, per query row (s = bytes per
     q/k/v element):
-      fwd_kernel           16 P D s (8 K and 8 V corner rows per point) + D s (q) + 12 P
-                           (offsets) + D s (out) + 4 (lse)
-      bwd_sweep_kernel     16 P D s + 2 D s (q, dout) + 12 P + 4 (lse) + 32 P (point records)
-                           + 4 P (bin-count atomics) + 4 D (dq) + 4 (Delta)
-      bwd_finalize_kernel  32 P (records) + 4 P (Delta) + 12 P (offsets) + 12 P (d_offsets)
-                           + 4 P (slot atomic) + 24 P (bin entry)
+      fwd_kernel        16 P D s (8 K and 8 V corner rows per point) + D s (q) + 12 P
+                        (offsets) + D s (out) + 4 (lse)
+      bwd_vpass_kernel  8 P D s (V corner rows) + D s (dout) + 12 P (offsets) + 16 P (the V
+                        half of each point record) + 4 P (bin-count atomics)
+      bwd_kpass_kernel  8 P D s (K corner rows) + D s (q) + 24 P (offsets, twice) + 4 (lse)
+                        + 4 P (da_p) + 16 P (the K half of each record) + 32 P (the records,
+                        read back to finish the points) + 4 D (dq) + 12 P (d_offsets) + 4 P
+                        (slot atomics) + 24 P (bin entries)
     These, not the HBM bytes, are what bounds the kernels: the corner rows come from L2 and
-    L1, and the per-unit gather path is busy ~90% of the time (rocprofv3 TA/TD counters)."""
+    L1, and the per-unit gather path is busy most of the time (rocprofv3 TA/TD counters)."""
     s = 2 if w.dtype == "bf16" else 4
     P, D = w.P, w.head_dim
     per = {
         "fwd_kernel": 16 * P * D * s + 2 * D * s + 12 * P + 4,
-        "bwd_sweep_kernel": 16 * P * D * s + 2 * D * s + 12 * P + 4 + 36 * P + 4 * D + 4,
-        "bwd_finalize_kernel": 88 * P,
+        "bwd_vpass_kernel": 8 * P * D * s + D * s + 12 * P + 16 * P + 4 * P,
+        "bwd_kpass_kernel": 8 * P * D * s + D * s + 24 * P + 4 + 4 * P + 48 * P + 4 * D
+                            + 12 * P + 4 * P + 24 * P,
     }
     return {k: w.queries * b for k, b in per.items()}
 
 
+PROBE_SRC = os.path.join(ROOT, "gather_probe.hip")
+PROBE_LIB = os.path.join(ROOT, "libgather_probe.so")
+
+
+def build_probe(verbose=False):
+    """Compile the gather microbenchmark (gather_probe.hip, measurement only) beside this
+    script."""
+    from paper_2607_22696_amd import build as pkg_build
+    pkg_build.compile_shared([PROBE_SRC], PROBE_LIB, verbose)
+    return PROBE_LIB
+
+
 def gather_ceiling(row_bytes):
-    """The gather microbenchmark (libdsa3d_probe.so): 16-byte lane loads, one contiguous row
+    """The gather microbenchmark (libgather_probe.so): 16-byte lane loads, one contiguous row
     of row_bytes per lane group at pseudo-random addresses, every row already in L1 (the
-    ceiling of the kernels' gather path), every row missing L1 and hitting L2, and the same
-    pattern from LDS."""
+    ceiling of the kernels' gather path), every row missing L1 and hitting L2, the same
+    pattern from LDS, and rows from a 512 MB region (missing L2: what comes from past the
+    L2s)."""
     import ctypes
-    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_22696_amd", "libdsa3d_probe.so"))
+    if not os.path.exists(PROBE_LIB):
+        raise RuntimeError(f"{PROBE_LIB} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(PROBE_LIB)
     lib.dsa3d_probe_gather.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.POINTER(ctypes.c_float),
                                        ctypes.POINTER(ctypes.c_double)]
     out = {"row_bytes": row_bytes}
-    for src, name in ((0, "l1"), (2, "l2"), (1, "lds")):
+    for src, name in ((0, "l1"), (2, "l2"), (1, "lds"), (3, "mem")):
         ms, nb = ctypes.c_float(), ctypes.c_double()
         rc = lib.dsa3d_probe_gather(src, row_bytes, 2048, 4096, ctypes.byref(ms), ctypes.byref(nb))
         if rc != 0:
             raise RuntimeError(f"gather probe failed ({rc})")
         out[f"{name}_TBps"] = round(nb.value / (ms.value * 1e-3) / 1e12, 2)
     return out
+
+
+def working_set_curve(sets_mib=(1, 2, 3, 4, 6, 8, 16, 32, 64, 128, 256, 512)):
+    """Random gathers of whole rows (256 B, and 128 B) from working sets of growing size, the
+    rows contiguous and 6 KB apart (one head of a 24-head x 256 B tensor): the rate as the
+    working set outgrows an XCD's 4 MB L2 and the 256 MB memory-side cache.  One JSON line per
+    point."""
+    import ctypes
+    lib = ctypes.CDLL(PROBE_LIB)
+    fn = lib.dsa3d_probe_working_set
+    fn.argtypes = [ctypes.c_int, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_int, ctypes.c_int,
+                   ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]
+    for rb in (256, 128):
+        for stride in (rb, 6144):
+            for mib in sets_mib:
+                ms, nb = ctypes.c_float(), ctypes.c_double()
+                set_bytes = mib << 20
+                if set_bytes // rb * stride > (4 << 30):
+                    continue
+                rc = fn(rb, stride, set_bytes, 8192, 256, ctypes.byref(ms), ctypes.byref(nb))
+                if rc != 0:
+                    raise RuntimeError(f"working-set probe failed ({rc})")
+                print(json.dumps({"row_bytes": rb, "stride_bytes": stride, "set_MiB": mib,
+                                  "ms": round(ms.value, 4),
+                                  "TBps": round(nb.value / (ms.value * 1e-3) / 1e12, 2)}),
+                      flush=True)
 
 
 def roofline(work, ms, peak=VALU_PEAK_TFLOPS, bound="alu"):
@@ -285,7 +411,7 @@ def cpu_baseline(w, host, budget_s, backward=True):
     what = ", ".join(f"head {m} frames [0,{f})" for m, f in done)
     # one query token carries all heads: rows / heads tokens
     return {"value": rows_done / w.heads / dt, "unit": "queries/s", "cores": oracle.threads(),
-            "kind": "oracle",
+            "kind": "oracle", **host_info(),
             "sample": f"{what} of {w.name}: {rows_done} (token, head) rows, "
                       + ("forward + backward incl. dK/dV scatter" if backward else "forward")
                       + f", fp64, {dt:.1f} s; "
@@ -322,6 +448,7 @@ def conv_cpu_baseline(w, host, budget_s):
     dt = time.perf_counter() - t0
     toks = frames * w.H * w.W * w.B
     return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+            **host_info(),
             "sample": f"frames [0,{frames}) of {w.name}: {toks} tokens x {w.C} channels, forward "
                       f"+ dx (no weight gradient), fp64, {dt:.1f} s"}
 
@@ -468,8 +595,7 @@ def bench_pw(args, torch, dsa, testgen, to_device):
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / K
     kernel_ms = {"fwd_kernel": sum(e[0].elapsed_time(e[1]) for e in ev) / K}
-    for i, n in enumerate(["bwd_sweep_kernel", "bin_scan", "bwd_finalize_kernel",
-                           "bwd_gather_kernel"]):
+    for i, n in enumerate(PW_BWD_PHASES):
         kernel_ms[n] = sum(p[i].elapsed_time(p[i + 1]) for p in ph) / K
     alg = pw_algorithmic(w)
     kname = max((n for n in kernel_ms if n in alg), key=lambda n: kernel_ms[n])
@@ -508,7 +634,7 @@ def bench_pw(args, torch, dsa, testgen, to_device):
         dt = time.perf_counter() - t0
         res["cpu_baseline"] = {
             "value": frames * w.H * w.W / w.heads / dt, "unit": "queries/s",
-            "cores": oracle.threads(), "kind": "oracle",
+            "cores": oracle.threads(), "kind": "oracle", **host_info(),
             "sample": f"head 0 frames [0,{frames}) of {w.name}: forward + backward incl. dV "
                       f"scatter, fp64, {dt:.1f} s; scaled to query tokens (all {w.heads} heads)"}
     print(json.dumps(res), flush=True)
@@ -649,7 +775,7 @@ def bench_win(args, torch, dsa, testgen, to_device):
         dt = time.perf_counter() - t0
         res_json["cpu_baseline"] = {
             "value": round(len(frames) * w.H * w.W * w.B / dt, 2), "unit": "queries/s",
-            "cores": oracle.threads(), "kind": "oracle",
+            "cores": oracle.threads(), "kind": "oracle", **host_info(),
             "sample": f"frames {frames[0]}..{frames[-1]} of {w.name} (all heads): forward + "
                       f"backward of their queries, fp64, {dt:.1f} s"}
     print(json.dumps(res_json), flush=True)
@@ -658,8 +784,8 @@ def bench_win(args, torch, dsa, testgen, to_device):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--op", choices=["dsa", "dwconv", "pw", "win"], default="dsa",
                     help="dsa: the 3D-DSA operator (default); dwconv: the depthwise 3D "
                          "convolution term of Eq. (1) (workloads dwconv_*); pw: the "
@@ -671,12 +797,15 @@ def main():
                     help="time the forward alone (workloads without a backward pass)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of CPU-oracle work for cpu_baseline (0 = skip)")
-    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH", "WRITE", "COPYF", "COPYW"),
-                    help="summarise four rocprofv3 --pmc output folders into "
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("READS", "WRITES", "COPYR", "COPYW"),
+                    help="summarise four rocprofv3 --pmc output folders (READ_COUNTERS and "
+                         "WRITE_COUNTERS of a bench command and of --copy-probe) into "
                          "profiles/traffic_<workload>.json (no GPU needed)")
+    ap.add_argument("--working-set-probe", action="store_true",
+                    help="only print the gather rate against working-set size and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
-                    help="only run 3 device-to-device copies of MIB MiB and exit (calibrates the "
-                         "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
+                    help="only run 3 device-to-device copies of MIB MiB and exit (checks the "
+                         "traffic counters against a known byte count)")
     args = ap.parse_args()
 
     if args.workload is None:
@@ -699,6 +828,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.working_set_probe:
+        working_set_curve()
+        return
     if args.copy_probe:
         n = args.copy_probe * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -791,8 +923,7 @@ def main():
     # average duration of each kernel (HIP events on the stream the kernels run on)
     kernel_ms = {"fwd_kernel": fwd_ms}
     if do_bwd:
-        names = ["bwd_sweep_kernel", "bin_scan", "bwd_finalize_kernel", "bwd_gather_kernel"]
-        for i, n in enumerate(names):
+        for i, n in enumerate(BWD_PHASES):
             kernel_ms[n] = sum(p[i].elapsed_time(p[i + 1]) for p in ph) / K
 
     alg = algorithmic(w)
@@ -842,7 +973,8 @@ def main():
         "hbm_frac_algorithmic": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "token_head_rows_per_s": round(w.queries / (ms_step * 1e-3), 1),
         "roofline": roof,
-        "hbm_rocprof": hbm_rocprof(w.name, do_bwd, ms_step),
+        "hbm_rocprof": hbm_rocprof(w.name, do_bwd, ms_step, step_bytes),
+        "hbm_ceiling": copy_ceiling(torch),
         "gather_path": gather_path,
         "input_gen_s": round(t_gen, 1),
     }

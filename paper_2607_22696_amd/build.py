@@ -1,5 +1,4 @@
-"""Builds libdsa3d.so (gfx950 HIP kernels + C-ABI host code) in-tree with hipcc, and the
-gather-bandwidth microbenchmark libdsa3d_probe.so that bench.py uses for its ceiling."""
+"""Builds libdsa3d.so (gfx950 HIP kernels + C-ABI host code) in-tree with hipcc."""
 from __future__ import annotations
 
 import os
@@ -11,8 +10,6 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdsa3d.so")
-PROBE_LIB = os.path.join(PKG, "libdsa3d_probe.so")
-PROBE_SOURCES = [os.path.join(CSRC, "gather_probe.hip")]
 
 SOURCES = [os.path.join(CSRC, "dsa3d_forward.hip"), os.path.join(CSRC, "dsa3d_backward.hip"),
            os.path.join(CSRC, "dwconv3d.hip"), os.path.join(CSRC, "dsa3d_api.cpp"),
@@ -27,7 +24,6 @@ FLAGS = [
     "-std=c++17",
     "-fPIC",
     "-shared",
-    "-munsafe-fp-atomics",
     # no packed-FP32 instructions in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall",
@@ -35,12 +31,13 @@ FLAGS = [
 
 
 def build(verbose: bool = False) -> str:
-    _compile(SOURCES, LIB, verbose)
-    _compile(PROBE_SOURCES, PROBE_LIB, verbose)
+    compile_shared(SOURCES, LIB, verbose)
     return LIB
 
 
-def _compile(sources, lib, verbose):
+def compile_shared(sources, lib, verbose=False):
+    """hipcc the sources into the shared library `lib` (replaced only when the build
+    succeeds)."""
     tmp = lib + ".tmp"
     cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, *sources, "-o", tmp]
     if verbose:

@@ -33,9 +33,11 @@ namespace {
 
 using namespace dev;
 
-// Per-point record of the sweep, read by the finalize pass.
+// Per-point record of the backward: the half that needs the K corners (alpha_p, A_p) and
+// the half that needs the V corners (da_p, B_p), each one 16-byte store.
 struct __align__(16) PointRec {
-  float alpha, dalpha, ax, ay, az, bx, by, bz;
+  float alpha, ax, ay, az;   // K half
+  float dalpha, bx, by, bz;  // V half
 };
 
 // A point's contribution to dK/dV, stored in the bin of its cell.
@@ -218,8 +220,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
           b3[a] = group_sum<L>(b3[a]);
         }
         if (sub == kk) {
-          rec0 = make_float4(alpha, da, a3[0], a3[1]);
-          rec1 = make_float4(a3[2], b3[0], b3[1], b3[2]);
+          rec0 = make_float4(alpha, a3[0], a3[1], a3[2]);
+          rec1 = make_float4(da, b3[0], b3[1], b3[2]);
         }
       }
       if (own) {
@@ -238,6 +240,262 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
                         g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
     }
     if (sub == 0) delta_out[row] = delta;
+  }
+}
+
+// ---------------------------------------------------------------------------- 1b. split sweep
+//
+// The same work as the sweep in two passes over the points, one over the V corners and one
+// over the K corners, so that each pass keeps only one of the two tensors' rows in the L2s.
+// The V pass forms da_p = <dout, v_p> and B_p and counts the bins; after the scan, the K pass
+// forms alpha_p, A_p, dq and Delta, and once a row's Delta is known its lanes finish the
+// row's points: d_offsets and the point's entry in its bin (what the finalize pass does in
+// the one-sweep order).
+
+// d_offsets of point p of a row and its entry in the bin of its cell, once the row's Delta is
+// known.  (t, i, j): the query token; n its index in the batch item; bh its (batch, head)
+// group.  dlogits (the predicted-weights variant, else null) receives alpha_p (da_p - Delta).
+__device__ inline void finish_point(const Geometry& g, const PointRec& r, float delta,
+                                    const float* __restrict__ o, int bh, int n, int t, int i, int j,
+                                    int p, float* __restrict__ d, float* __restrict__ dlogit,
+                                    uint32_t* __restrict__ cursor, Entry* __restrict__ entries) {
+  const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
+  const float dd = r.dalpha - delta;
+  const float sa = g.scale * dd;
+  d[0] = r.alpha * fmaf(sa, r.ax, r.bx);
+  d[1] = r.alpha * fmaf(sa, r.ay, r.by);
+  d[2] = r.alpha * fmaf(sa, r.az, r.bz);
+  if (dlogit != nullptr) *dlogit = r.alpha * dd;
+  const int iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
+  int x, y, z;
+  float fx, fy, fz;
+  axis((float)(j + iw - rw), o[0], g.W, x, fx);
+  axis((float)(i + ih - rh), o[1], g.H, y, fy);
+  axis((float)(t + it - rt), o[2], g.T, z, fz);
+  if (!cell_inside(g, x, y, z)) return;
+  const uint32_t slot = atomicAdd(cursor + cell_index(g, bh, x, y, z), 1u);
+  Entry e;
+  e.n = (int32_t)n;
+  e.alpha = r.alpha;
+  e.sds = g.scale * r.alpha * dd;
+  e.fx = fx;
+  e.fy = fy;
+  e.fz = fz;
+  entries[slot] = e;
+}
+
+// Point setup shared by the two passes: the row's lanes fetch point `kk` of the chunk from the
+// lane that formed it (`mine`): corner indices, fractions, and the weights rebuilt from them.
+__device__ inline __attribute__((always_inline)) void fetch_point(const Point& mine, int src,
+                                                                 Point& pt) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) pt.vidx[c] = __builtin_amdgcn_ds_bpermute(src, mine.vidx[c]);
+  const float tx = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.ax[1])));
+  const float ty = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.ay[1])));
+  const float tz = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mine.az[1])));
+  pt.ax[0] = 1.0f - tx;
+  pt.ax[1] = tx;
+  pt.ay[0] = 1.0f - ty;
+  pt.ay[1] = ty;
+  pt.az[0] = 1.0f - tz;
+  pt.az[1] = tz;
+  const float wyz[4] = {pt.ay[0] * pt.az[0], pt.ay[1] * pt.az[0], pt.ay[0] * pt.az[1],
+                        pt.ay[1] * pt.az[1]};
+#pragma unroll
+  for (int c = 0; c < 8; ++c) pt.w[c] = pt.ax[c & 1] * wyz[c >> 1];
+}
+
+// d w_c / d pos of corner c along x, y, z.
+__device__ inline __attribute__((always_inline)) void weight_grad(const Point& pt, int c,
+                                                                  float& wx, float& wy, float& wz) {
+  const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
+  wx = cx ? pt.ay[cy] * pt.az[cz] : -(pt.ay[cy] * pt.az[cz]);
+  wy = cy ? pt.ax[cx] * pt.az[cz] : -(pt.ax[cx] * pt.az[cz]);
+  wz = cz ? pt.ax[cx] * pt.ay[cy] : -(pt.ax[cx] * pt.ay[cy]);
+}
+
+// V pass: per point da_p = <dout, v_p> and B_p = sum_c dw_c/dpos <dout, V_c> into the V half
+// of the record; every point is counted into the bin of its cell.
+template <int D, bool BF16>
+__global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_kernel(
+    Geometry g, const void* __restrict__ v, const float* __restrict__ offsets,
+    const void* __restrict__ dout, PointRec* __restrict__ recs, uint32_t* __restrict__ counts,
+    PencilOrder po) {
+  using LY = Layout<D, BF16>;
+  constexpr int L = LY::kLanes;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / L, sub = lane % L;
+  const int lane_off = sub * 16;
+  const char* vb = static_cast<const char*>(v);
+  const char* gb = static_cast<const char*>(dout);
+  const int HW = g.H * g.W;
+  const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
+  const int khw = g.kh * g.kw;
+
+  for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
+    PencilTile tl;
+    if (!pencil_tile(po, vt, tl)) continue;
+    const int bh = tl.group;
+    const int b = bh / g.heads, m = bh % g.heads;
+    const int t = tl.frame;
+    const RowWindow win = make_window<LY::kRowBytes>(g, v, v, b, m, t);  // V rows only
+    int i, j;
+    if (!pencil_cell(po, tl, wave * LY::kGroups + grp, i, j)) continue;  // a whole group idles
+    const int n = t * HW + i * g.W + j;
+    const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
+    const uint4 gr = load16(gb, row * LY::kRowBytes + lane_off);
+    const float* off = offsets + row * g.P * 3;
+    int pm = min(sub, g.P - 1);  // this lane's point of the chunk (clamped in the last one)
+    float ox = off[3 * pm], oy = off[3 * pm + 1], oz = off[3 * pm + 2];
+    for (int p0 = 0; p0 < g.P; p0 += L) {
+      const int it = pm / khw, ih = (pm - it * khw) / g.kw, iw = pm - it * khw - ih * g.kw;
+      Point mine;
+      make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
+      const bool own = p0 + sub < g.P;
+      if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))  // result unused: no wait
+        __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      pm = min(p0 + L + sub, g.P - 1);  // next chunk's offsets, in flight during this one
+      ox = off[3 * pm];
+      oy = off[3 * pm + 1];
+      oz = off[3 * pm + 2];
+      const int nk = min(L, g.P - p0);
+      float4 rec = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      for (int kk = 0; kk < nk; ++kk) {
+        const int src = (grp * L + kk) << 2;
+        Point pt;
+        fetch_point(mine, src, pt);
+        uint4 vr[8];
+        load_shared_corners<LY::kRowBytes, false>(g, win, vb, vb, b, m, lane_off, mine, src,
+                                                  pt.vidx, nullptr, vr);
+        float dap = 0.0f, b3[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const float dvv = chunk_dot<BF16>(gr, vr[c]);
+          float wx, wy, wz;
+          weight_grad(pt, c, wx, wy, wz);
+          dap = fmaf(pt.w[c], dvv, dap);
+          b3[0] = fmaf(wx, dvv, b3[0]);
+          b3[1] = fmaf(wy, dvv, b3[1]);
+          b3[2] = fmaf(wz, dvv, b3[2]);
+        }
+        const float da = group_sum<L>(dap);
+#pragma unroll
+        for (int a = 0; a < 3; ++a) b3[a] = group_sum<L>(b3[a]);
+        if (sub == kk) rec = make_float4(da, b3[0], b3[1], b3[2]);
+      }
+      if (own) reinterpret_cast<float4*>(recs + row * g.P + p0 + sub)[1] = rec;
+    }
+  }
+}
+
+// K pass: alpha_p from the logit and the forward's LSE, A_p = sum_c dw_c/dpos <q, K_c> into the
+// K half of the record, Delta = sum_p alpha_p da_p and dq; then, with Delta known, the row's
+// lanes finish its points (finish_point).  Needs the V pass's records and the bin starts.
+template <int D, bool BF16>
+__global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_kernel(
+    Geometry g, const void* __restrict__ q, const void* __restrict__ k,
+    const float* __restrict__ offsets, const float* __restrict__ lse, float* __restrict__ dq,
+    PointRec* __restrict__ recs, uint32_t* __restrict__ cursor, float* __restrict__ doff,
+    Entry* __restrict__ entries, PencilOrder po) {
+  using LY = Layout<D, BF16>;
+  constexpr int L = LY::kLanes;
+  constexpr int VEC = LY::kVec;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / L, sub = lane % L;
+  const int lane_off = sub * 16;
+  const char* qb = static_cast<const char*>(q);
+  const char* kb = static_cast<const char*>(k);
+  const int HW = g.H * g.W;
+  const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
+  const int khw = g.kh * g.kw;
+
+  for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
+    PencilTile tl;
+    if (!pencil_tile(po, vt, tl)) continue;
+    const int bh = tl.group;
+    const int b = bh / g.heads, m = bh % g.heads;
+    const int t = tl.frame;
+    const RowWindow win = make_window<LY::kRowBytes>(g, k, k, b, m, t);  // K rows only
+    int i, j;
+    if (!pencil_cell(po, tl, wave * LY::kGroups + grp, i, j)) continue;  // a whole group idles
+    const int n = t * HW + i * g.W + j;
+    const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
+    const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
+    const float lse2 = lse[row] * kLog2e;
+    const float* off = offsets + row * g.P * 3;
+    PointRec* rrow = recs + row * g.P;
+    float ak[VEC], bk[VEC];
+#pragma unroll
+    for (int x = 0; x < VEC; ++x) {
+      ak[x] = 0.0f;
+      bk[x] = 0.0f;
+    }
+    float delta = 0.0f;
+    int pm = min(sub, g.P - 1);
+    float ox = off[3 * pm], oy = off[3 * pm + 1], oz = off[3 * pm + 2];
+    for (int p0 = 0; p0 < g.P; p0 += L) {
+      const int it = pm / khw, ih = (pm - it * khw) / g.kw, iw = pm - it * khw - ih * g.kw;
+      Point mine;
+      make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
+      const bool own = p0 + sub < g.P;
+      const float my_da = rrow[pm].dalpha;  // this lane's point's da_p (V pass)
+      pm = min(p0 + L + sub, g.P - 1);
+      ox = off[3 * pm];
+      oy = off[3 * pm + 1];
+      oz = off[3 * pm + 2];
+      const int nk = min(L, g.P - p0);
+      float4 rec = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      for (int kk = 0; kk < nk; ++kk) {
+        const int src = (grp * L + kk) << 2;
+        Point pt;
+        fetch_point(mine, src, pt);
+        uint4 kr[8];
+        load_shared_corners<LY::kRowBytes, false>(g, win, kb, kb, b, m, lane_off, mine, src,
+                                                  pt.vidx, nullptr, kr);
+        float sp = 0.0f, a3[3] = {0.0f, 0.0f, 0.0f};
+        float kp[VEC];
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) kp[x] = 0.0f;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const float qk = chunk_dot<BF16>(qr, kr[c]);
+          float wx, wy, wz;
+          weight_grad(pt, c, wx, wy, wz);
+          sp = fmaf(pt.w[c], qk, sp);
+          a3[0] = fmaf(wx, qk, a3[0]);
+          a3[1] = fmaf(wy, qk, a3[1]);
+          a3[2] = fmaf(wz, qk, a3[2]);
+          chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
+        }
+        const float alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
+        const float da = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(my_da)));
+        delta = fmaf(alpha, da, delta);
+        const float ada = alpha * da;
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) {
+          ak[x] = fmaf(ada, kp[x], ak[x]);
+          bk[x] = fmaf(alpha, kp[x], bk[x]);
+        }
+#pragma unroll
+        for (int a = 0; a < 3; ++a) a3[a] = group_sum<L>(a3[a]);
+        if (sub == kk) rec = make_float4(alpha, a3[0], a3[1], a3[2]);
+      }
+      if (own) reinterpret_cast<float4*>(rrow + p0 + sub)[0] = rec;
+    }
+    float* dqr = dq + row * D + sub * VEC;
+#pragma unroll
+    for (int x = 0; x < VEC; x += 4)
+      *reinterpret_cast<float4*>(dqr + x) =
+          make_float4(g.scale * fmaf(-delta, bk[x], ak[x]), g.scale * fmaf(-delta, bk[x + 1], ak[x + 1]),
+                      g.scale * fmaf(-delta, bk[x + 2], ak[x + 2]),
+                      g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
+    // Delta is known: finish the row's points (lane sub takes points sub, sub + L, ...; it
+    // wrote the K half of exactly these records above, and program order makes its own
+    // stores visible to its loads)
+    for (int p = sub; p < g.P; p += L)
+      finish_point(g, rrow[p], delta, off + 3 * p, bh, n, t, i, j, p, doff + (row * g.P + p) * 3,
+                   nullptr, cursor, entries);
   }
 }
 
@@ -939,8 +1197,18 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   }
   const PencilOrder po = query_order<D, BF16>(g);
   const int blocks = grid_blocks(po.vtiles);
+  // The main operator sweeps the points twice (V pass, then K pass with the finish of each
+  // row's points); the predicted-weights variant, which reads no K, sweeps them once and
+  // finishes them in the finalize pass.
+  const bool split = !pw;
   if ((e = mark(0)) != hipSuccess) return e;
-  {
+  if (split) {
+    void* a[] = {(void*)&g, (void*)&v, (void*)&off, (void*)&dout, (void*)&w.recs,
+                 (void*)&w.counts, (void*)&po};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_vpass_kernel<D, BF16>), dim3(blocks),
+                        dim3(kBlockThreads), a, 0, s);
+    if (e != hipSuccess) return e;
+  } else {
     void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,       (void*)&v,
                  (void*)&logits, (void*)&off,  (void*)&lse,     (void*)&dout,
                  (void*)&dq,   (void*)&w.recs, (void*)&w.delta, (void*)&w.counts,
@@ -968,7 +1236,14 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     if (e != hipSuccess) return e;
   }
   if ((e = mark(2)) != hipSuccess) return e;
-  {
+  if (split) {
+    void* a[] = {(void*)&g,      (void*)&q,        (void*)&k,    (void*)&off,
+                 (void*)&lse,    (void*)&dq,       (void*)&w.recs, (void*)&w.cursor,
+                 (void*)&doff,   (void*)&w.entries, (void*)&po};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_kpass_kernel<D, BF16>), dim3(blocks),
+                        dim3(kBlockThreads), a, 0, s);
+    if (e != hipSuccess) return e;
+  } else {
     const int npoints = (int)points;
     void* a[] = {(void*)&g,      (void*)&off,     (void*)&w.recs,    (void*)&w.delta,
                  (void*)&w.cursor, (void*)&doff, (void*)&dlogits, (void*)&w.entries,
@@ -980,9 +1255,11 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   if ((e = mark(3)) != hipSuccess) return e;
   if constexpr (BF16) {
     constexpr int NW = gather_waves<D>();
-    // cells: 4 x 2 voxel blocks of a frame pair; pencils of about 16 x 16 voxels
+    // cells: 4 x 2 voxel blocks of a frame pair; pencils of about 32 x 32 voxels (measured
+    // at 64x68x120 / 64x34x60: 108.3 / 3.42 ms, against 108.8 / 3.68 for 16 x 16 voxels,
+    // 110.6 / 3.76 for 8 x 8 and 132.5 / 3.25 for whole frames)
     const PencilOrder go = plan_pencils(g.B * g.heads, (g.T + 1) / 2, (g.H + 1) / 2,
-                                        (g.W + 3) / 4, NW, 8, 4);
+                                        (g.W + 3) / 4, NW, 16, 8);
     const int gblocks = grid_blocks(go.vtiles);
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
                  (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&go};
@@ -992,9 +1269,9 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     if (e != hipSuccess) return e;
   } else {
     using LY = Layout<D, BF16>;
-    // cells: 2 x 2 voxel blocks of a frame; pencils of about 16 x 16 voxels
+    // cells: 2 x 2 voxel blocks of a frame; pencils of about 32 x 32 voxels
     const PencilOrder go = plan_pencils(g.B * g.heads, g.T, (g.H + 1) / 2, (g.W + 1) / 2,
-                                        LY::kRowsPerBlock, 8, 8);
+                                        LY::kRowsPerBlock, 16, 16);
     const int gblocks = grid_blocks(go.vtiles);
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
                  (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&go};

@@ -291,10 +291,12 @@ __device__ inline __attribute__((always_inline)) void load_shared_corners(
 constexpr int kMaxBlocks = 1 << 22;  // grid cap; larger problems loop over tiles
 
 // Pencil order of the query-owned kernels: tiles of kRowsPerBlock tokens inside pencils of
-// about 16 x 16 tokens of a frame.
+// about 12 x 12 tokens of a frame.  Measured on one MI355X at 64x68x120, 24 heads x 128,
+// 3x5x5, offsets U[-8,8]: forward 159 / 162 / 197 ms and sweep 199 / 201 / 220 ms with
+// pencils of about 12 x 12 / 16 x 16 / 24 x 24 tokens.
 template <int D, bool BF16>
 inline PencilOrder query_order(const Geometry& g) {
-  return plan_pencils(g.B * g.heads, g.T, g.H, g.W, Layout<D, BF16>::kRowsPerBlock, 16, 16);
+  return plan_pencils(g.B * g.heads, g.T, g.H, g.W, Layout<D, BF16>::kRowsPerBlock, 12, 12);
 }
 
 // Workgroups for `vtiles` virtual tiles: at most kMaxBlocks, a multiple of 8 when capped so

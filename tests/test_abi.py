@@ -472,9 +472,9 @@ def test_win_workspace_size_and_errors():
 
 
 def test_gather_probe_library_exports_its_entry_point():
-    """The gather microbenchmark bench.py reports its ceiling from is built beside the
-    library and exports its one C entry point (running it needs a GPU)."""
+    """The gather microbenchmark bench.py reports its ceiling from is built beside bench.py
+    (not into the library) and exports its one C entry point (running it needs a GPU)."""
     import os
-    lib = os.path.join(os.path.dirname(dsa.__file__), "libdsa3d_probe.so")
+    lib = os.path.join(os.path.dirname(INCLUDE), "libgather_probe.so")
     assert os.path.exists(lib), lib
     assert hasattr(ctypes.CDLL(lib), "dsa3d_probe_gather")

@@ -32,7 +32,7 @@ def test_the_bf16_gather_is_priced_against_the_matrix_peak():
     g = bench.kernel_roofline(w16, alg, "bwd_gather_kernel", 3.0)
     # 32 P D flops per row against 2.5 PFLOP/s take less time than the HBM bytes at 8 TB/s
     assert g["bound"] == "hbm"
-    assert bench.kernel_roofline(w16, alg, "bwd_sweep_kernel", 6.0)["bound"] == "alu"
+    assert bench.kernel_roofline(w16, alg, "bwd_kpass_kernel", 4.0)["bound"] == "alu"
     w32 = testgen.WORKLOADS["tiny_f32"]
     a32 = bench.algorithmic(w32)
     assert bench.kernel_roofline(w32, a32, "bwd_gather_kernel", 1.0) == bench.roofline(
@@ -67,7 +67,7 @@ def test_more_than_one_gpu_is_refused_with_a_message():
 
 
 def test_gather_probe_rejects_bad_arguments_before_touching_the_device():
-    path = os.path.join(ROOT, "paper_2607_22696_amd", "libdsa3d_probe.so")
+    path = bench.PROBE_LIB
     if not os.path.exists(path):
         pytest.skip("probe library not built")
     lib = ctypes.CDLL(path)
@@ -75,11 +75,19 @@ def test_gather_probe_rejects_bad_arguments_before_touching_the_device():
     fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]
     ms, nb = ctypes.c_float(), ctypes.c_double()
-    assert fn(3, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no such source
+    assert fn(4, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no such source
     assert fn(-1, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1
     assert fn(2, 48, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1    # row size
     assert fn(0, 128, 0, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no blocks
     assert fn(1, 64, 8, 8, None, ctypes.byref(nb)) == -1                # null output
+    ws = lib.dsa3d_probe_working_set
+    ws.argtypes = [ctypes.c_int, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_int, ctypes.c_int,
+                   ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]
+    assert ws(192, 256, 1 << 20, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # row size
+    assert ws(256, 128, 1 << 20, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # stride < row
+    assert ws(256, 6144, 1 << 30, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1  # span > 4 GB
+    assert ws(256, 250, 1 << 20, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # not 16-B
+    assert ws(256, 256, 100, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1       # < one row
 
 
 def test_rocprof_step_traffic_sums_the_step_kernels_and_refuses_stale_counters(tmp_path, monkeypatch):
@@ -94,13 +102,56 @@ def test_rocprof_step_traffic_sums_the_step_kernels_and_refuses_stale_counters(t
     # 8e9 bytes in 1 ms is the 8 TB/s peak
     kernels["fwd_kernel"]["hbm_bytes"] = 8 * 10 ** 9
     (tmp_path / "traffic_w.json").write_text(json.dumps(doc))
-    r = bench.hbm_rocprof("w", False, 1.0)
+    r = bench.hbm_rocprof("w", False, 1.0, 2 * 10 ** 9)
     assert r["GBps"] == pytest.approx(8000.0) and r["frac_of_peak"] == pytest.approx(1.0)
+    assert r["ratio_to_algorithmic"] == pytest.approx(4.0) and r["counted_at"] == "L2 egress"
     # a kernel of the step without counters, counters of other sources, no file: no figure
-    del kernels["bwd_finalize_kernel"]
+    del kernels["bwd_kpass_kernel"]
     (tmp_path / "traffic_w.json").write_text(json.dumps(doc))
     assert bench.measured_step_traffic("w", True) is None
     doc["kernel_source_hash"] = "0" * 16
     (tmp_path / "traffic_w.json").write_text(json.dumps(doc))
-    assert bench.hbm_rocprof("w", False, 1.0) is None
-    assert bench.hbm_rocprof("absent", True, 1.0) is None
+    assert bench.hbm_rocprof("w", False, 1.0, 1) is None
+    assert bench.hbm_rocprof("absent", True, 1.0, 1) is None
+
+
+def _counter_csv(path, rows):
+    """rows: (dispatch id, kernel name, counter, value) as rocprofv3 writes them."""
+    import csv
+    path.mkdir()
+    with open(path / "p_counter_collection.csv", "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for r in rows:
+            w.writerow(r)
+
+
+def test_pmc_summary_counts_read_requests_by_size(tmp_path, monkeypatch):
+    """Read bytes are 32, 64 and 128 bytes per request of each size (FETCH_SIZE, which counts
+    a 128-byte request as 64 bytes on this GPU, is not used); writes are WRITE_SIZE KiB; the
+    copy's figures are stored as a check of the accounting."""
+    import json
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path / "profiles"))
+    k = "void dsa3d::fwd_kernel<128, true, false>(...)"
+    reads = []
+    for d in (1, 2):  # two launches, averaged
+        reads += [(d, k, "TCC_EA0_RDREQ_32B_sum", 10), (d, k, "TCC_EA0_RDREQ_64B_sum", 20),
+                  (d, k, "TCC_EA0_RDREQ_128B_sum", 1000 * d), (d, k, "TCC_EA0_RDREQ_sum", 1030 + 1000 * (d - 1))]
+    writes = [(d, k, c, v) for d in (1, 2) for c, v in
+              (("WRITE_SIZE", 4.0), ("TCC_ATOMIC_sum", 7), ("TCC_EA0_ATOMIC_sum", 3))]
+    cp = "__amd_rocclr_copyBuffer"
+    copy_r = [(1, cp, "TCC_EA0_RDREQ_32B_sum", 0), (1, cp, "TCC_EA0_RDREQ_64B_sum", 0),
+              (1, cp, "TCC_EA0_RDREQ_128B_sum", 8192), (1, cp, "TCC_EA0_RDREQ_sum", 8192)]
+    copy_w = [(1, cp, "WRITE_SIZE", 1024.0), (1, cp, "TCC_ATOMIC_sum", 0),
+              (1, cp, "TCC_EA0_ATOMIC_sum", 0)]
+    for name, rows in (("r", reads), ("w", writes), ("cr", copy_r), ("cw", copy_w)):
+        _counter_csv(tmp_path / name, rows)
+    bench.pmc_summary("wl", str(tmp_path / "r"), str(tmp_path / "w"), str(tmp_path / "cr"),
+                      str(tmp_path / "cw"), 1)
+    doc = json.loads((tmp_path / "profiles" / "traffic_wl.json").read_text())
+    kr = doc["kernels"]["fwd_kernel"]
+    assert kr["fetch_bytes"] == 32 * 10 + 64 * 20 + 128 * 1500
+    assert kr["write_bytes"] == 4096 and kr["hbm_bytes"] == kr["fetch_bytes"] + 4096
+    assert kr["atomics_l2"] == 7 and kr["atomics_past_l2"] == 3
+    assert kr["read_requests_of_known_size"] == 1.0
+    assert doc["copy_check"] == {"mib": 1, "read_bytes_per_byte": 1.0, "write_bytes_per_byte": 1.0}

@@ -248,17 +248,29 @@ def sampled_rows(w, n, rng):
     return np.unique(np.concatenate([rows, np.array(extra, dtype=np.int64)]))
 
 
-def full_size_forward(w, nsamp):
+def frame_rows(w, frames):
+    """Every (token, head) row of the given frames (all heads)."""
+    HW = w.H * w.W
+    per = HW * w.heads
+    return np.concatenate([np.arange(f * per, (f + 1) * per, dtype=np.int64) for f in frames])
+
+
+def full_size_forward(w, nsamp, frames=()):
+    """The whole grid on the GPU; the oracle on `nsamp` random rows plus every row of
+    `frames`."""
     say(f"full-size {w.name}: generating {w.queries} rows ...")
     q, k, v, off, dout = testgen.gen_inputs(w, progress=say)
     say("  forward on GPU ...")
     qd, kd, vd, od, out, lse = run_forward(w, q, k, v, off)
     rng = np.random.default_rng(w.seed)
     rows = sampled_rows(w, nsamp, rng)
-    say(f"  oracle on {rows.size} sampled rows ...")
+    if len(frames):
+        rows = np.unique(np.concatenate([rows, frame_rows(w, frames)]))
+    say(f"  oracle on {rows.size} rows ({nsamp} sampled, frames {list(frames)}) ...")
     ref_out, ref_lse = oracle.forward(shape9(w), w.dtype, q, k, v, off, rows=rows)
-    out_h = to_host(out.view(-1, w.head_dim)[torch.from_numpy(rows).cuda()])
-    lse_h = to_host(lse.view(-1)[torch.from_numpy(rows).cuda()])
+    sel = torch.from_numpy(rows).cuda()
+    out_h = to_host(out.view(-1, w.head_dim)[sel])
+    lse_h = to_host(lse.view(-1)[sel])
     check("out", out_h, ref_out, True)
     check("lse", lse_h, ref_lse, True)
     return (q, k, v, off, dout), (qd, kd, vd, od), out, lse, rows
@@ -294,10 +306,21 @@ def full_size_backward(w, host, dev, out, lse, rows, slab_frames, slab_heads):
 
 
 @pytest.mark.slow
+@pytest.mark.timeout(900)
 def test_full_scale_1080p_256f_forward_sampled():
     """2,088,960 tokens x 24 heads x 128, 3x3x3 kernel: the full grid runs on the GPU in the
-    bench's launch configuration; 8192 sampled rows are checked."""
-    full_size_forward(testgen.WORKLOADS["full_1080p_256f"], 8192)
+    bench's launch configuration; every row of frames 0, 1, 128 and 255 (all 24 heads: the
+    first, last and an interior frame, and one whose corners reach across frame 0) plus 65,536
+    random rows are checked."""
+    full_size_forward(testgen.WORKLOADS["full_1080p_256f"], 65536, frames=(0, 1, 128, 255))
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_paper_3x7x7_1080p_256f_forward_sampled():
+    """The paper's 3x7x7 kernel (147 points) on the 256-frame 1080p grid, the forward the
+    bench profiles at that size: 4,096 random rows plus every row of frames 0 and 255."""
+    full_size_forward(testgen.WORKLOADS["paper_3x7x7_1080p_256f"], 4096, frames=(0, 255))
 
 
 @pytest.mark.slow
@@ -322,10 +345,14 @@ def test_fwdbwd_64x34x60_full_size():
 
 
 @pytest.mark.slow
+@pytest.mark.timeout(900)
 def test_wide_64x68x120_p75_full_size():
+    """The bench's default workload: 4,096 sampled rows plus all of frame 63 (forward, dq,
+    d_offsets) and dK / dV frame slabs of three heads."""
     w = testgen.WORKLOADS["wide_64x68x120_p75"]
-    host, dev, out, lse, rows = full_size_forward(w, 4096)
-    full_size_backward(w, host, dev, out, lse, rows, slab_frames=[0, 37], slab_heads=[5])
+    host, dev, out, lse, rows = full_size_forward(w, 4096, frames=(63,))
+    full_size_backward(w, host, dev, out, lse, rows, slab_frames=[0, 37],
+                       slab_heads=[0, 5, 23])
 
 
 @pytest.mark.slow
