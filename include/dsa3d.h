@@ -62,7 +62,9 @@ typedef enum {
   DSA3D_ERR_MISALIGNED = 4,    /* a pointer breaks the alignment rule above               */
   DSA3D_ERR_WORKSPACE = 5,     /* workspace NULL or smaller than the required size        */
   DSA3D_ERR_DEVICE = 6,        /* a HIP launch failed (the HIP error is not cleared)      */
-  DSA3D_ERR_ALIAS = 7          /* an output overlaps an input or another output           */
+  DSA3D_ERR_ALIAS = 7,         /* an output overlaps an input or another output           */
+  DSA3D_ERR_SCRATCH = 8        /* dsa3d_backward_noalloc: the problem needs more workspace
+                                  than DSA3D_NOALLOC_SCRATCH_BYTES                          */
 } dsa3d_status;
 
 typedef enum { DSA3D_F32 = 0, DSA3D_BF16 = 1 } dsa3d_dtype;
@@ -149,6 +151,26 @@ dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const v
                                   float* dv, float* d_offsets, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream,
                                   const hipEvent_t* events);
+
+/* Bytes of the fixed device scratch buffer of dsa3d_backward_noalloc (128 MiB). */
+#define DSA3D_NOALLOC_SCRATCH_BYTES (128u << 20)
+
+/* dsa3d_backward without a caller workspace and without any allocation, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  The workspace is a file-scope device array of the library,
+ * DSA3D_NOALLOC_SCRATCH_BYTES bytes on each GPU the library runs on, held until the process
+ * ends; its device address is looked up once per device on the first call there.  Arguments,
+ * results and checks are those of dsa3d_backward minus the workspace; a problem whose
+ * dsa3d_backward_workspace_size exceeds the scratch returns DSA3D_ERR_SCRATCH (that is about
+ * 2.2 million (row, point) pairs, e.g. 80,000 query rows with a 3x3x3 kernel) and enqueues
+ * nothing.  Every call on a GPU uses that GPU's one scratch array: calls that can overlap on
+ * one GPU (two streams, two host threads) race and must be serialised by the caller.  The
+ * library clears what must start at zero on `stream` itself (with a kernel, not a memset),
+ * so nothing from an earlier call carries over. */
+dsa3d_status dsa3d_backward_noalloc(const dsa3d_desc* desc, const void* q, const void* k,
+                                    const void* v, const float* offsets, const void* out,
+                                    const float* lse, const void* dout, float* dq, float* dk,
+                                    float* dv, float* d_offsets, hipStream_t stream);
 
 /* Static description of a status code (never NULL). */
 const char* dsa3d_status_string(dsa3d_status status);

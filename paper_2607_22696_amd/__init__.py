@@ -6,7 +6,7 @@ script and a thin binding; PyTorch is used only for device memory and streams.
 """
 from ._binding import (  # noqa: F401
     DSA3D_BACKWARD_PHASES, DSA3D_BF16, DSA3D_WIN_BACKWARD_PHASES, DSA3D_F32, DSA3D_MAX_POINTS, DSA3D_OK, EXPORTED, Dsa3dError,
-    dsa3d_abi_version, dsa3d_backward, dsa3d_backward_timed, dsa3d_backward_workspace_size,
+    dsa3d_abi_version, dsa3d_backward, dsa3d_backward_noalloc, dsa3d_backward_timed, dsa3d_backward_workspace_size,
     dsa3d_desc, dsa3d_dwconv3d_backward, dsa3d_dwconv3d_backward_workspace_size,
     dsa3d_dwconv3d_forward, dsa3d_dwconv_desc, dsa3d_forward, dsa3d_pw_backward,
     dsa3d_pw_backward_workspace_size, dsa3d_pw_forward, dsa3d_win_backward,

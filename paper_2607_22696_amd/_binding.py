@@ -21,6 +21,9 @@ DSA3D_ERR_MISALIGNED = 4
 DSA3D_ERR_WORKSPACE = 5
 DSA3D_ERR_DEVICE = 6
 DSA3D_ERR_ALIAS = 7
+DSA3D_ERR_SCRATCH = 8
+
+DSA3D_NOALLOC_SCRATCH_BYTES = 128 << 20
 
 DSA3D_F32 = 0
 DSA3D_BF16 = 1
@@ -30,7 +33,7 @@ DSA3D_BACKWARD_PHASES = 4
 
 DSA3D_DWCONV_MAX_TAPS = 128
 
-EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_timed",
+EXPORTED = ("dsa3d_forward", "dsa3d_backward", "dsa3d_backward_timed", "dsa3d_backward_noalloc",
             "dsa3d_backward_workspace_size", "dsa3d_status_string", "dsa3d_abi_version",
             "dsa3d_dwconv3d_forward", "dsa3d_dwconv3d_backward_workspace_size",
             "dsa3d_dwconv3d_backward", "dsa3d_pw_forward", "dsa3d_pw_backward_workspace_size",
@@ -88,6 +91,8 @@ def load():
         lib.dsa3d_backward_timed.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                              ctypes.c_size_t, vp, ctypes.POINTER(vp)]
         lib.dsa3d_backward_timed.restype = ctypes.c_int
+        lib.dsa3d_backward_noalloc.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        lib.dsa3d_backward_noalloc.restype = ctypes.c_int
         lib.dsa3d_pw_forward.argtypes = [pd, vp, vp, vp, vp, vp, vp]
         lib.dsa3d_pw_forward.restype = ctypes.c_int
         lib.dsa3d_pw_backward_workspace_size.argtypes = [pd]
@@ -188,6 +193,18 @@ def dsa3d_backward_timed(desc, q, k, v, offsets, out, lse, dout, dq, dk, dv, d_o
                                      _ptr(workspace), workspace_bytes, _stream(stream), arr)
     if check and st != DSA3D_OK:
         raise Dsa3dError(st, "dsa3d_backward_timed")
+    return st
+
+
+def dsa3d_backward_noalloc(desc, q, k, v, offsets, out, lse, dout, dq, dk, dv, d_offsets,
+                           stream=None, check=True) -> int:
+    """dsa3d_backward in the library's fixed scratch buffer (no workspace, no allocation)."""
+    st = load().dsa3d_backward_noalloc(ctypes.byref(desc) if desc is not None else None, _ptr(q),
+                                       _ptr(k), _ptr(v), _ptr(offsets), _ptr(out), _ptr(lse),
+                                       _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_offsets),
+                                       _stream(stream))
+    if check and st != DSA3D_OK:
+        raise Dsa3dError(st, "dsa3d_backward_noalloc")
     return st
 
 

@@ -12,6 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdsa3d.so")
 
 SOURCES = [os.path.join(CSRC, "dsa3d_forward.hip"), os.path.join(CSRC, "dsa3d_backward.hip"),
+           os.path.join(CSRC, "dsa3d_noalloc.hip"),
            os.path.join(CSRC, "dwconv3d.hip"), os.path.join(CSRC, "dsa3d_api.cpp"),
            os.path.join(CSRC, "dwconv3d_api.cpp"), os.path.join(CSRC, "winattn.hip"),
            os.path.join(CSRC, "winattn_api.cpp")]

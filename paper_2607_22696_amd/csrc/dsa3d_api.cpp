@@ -9,6 +9,7 @@
 #include <cstdint>
 
 #include "api_util.h"
+#include "backward_entry.h"
 #include "dsa3d_internal.h"
 
 namespace {
@@ -72,6 +73,59 @@ int window_frames(const Geometry& g, int row_bytes) {
   return (int)(frames < (uint64_t)g.T ? frames : (uint64_t)g.T);
 }
 
+// The backward bins every (query row, point) pair by its trilinear cell; bin ranks and entry
+// slots are 32-bit, so rows * P and the number of cells must stay below 2^31.
+static dsa3d_status check_backward_range(const dsa3d::Geometry& g, uint64_t rows) {
+  const uint64_t cells = (uint64_t)(g.T + 1) * (g.H + 1) * (g.W + 1) * g.B * g.heads;
+  if (rows * (uint64_t)g.P >= (1ull << 31) || cells >= (1ull << 31)) return DSA3D_ERR_INVALID_SHAPE;
+  return DSA3D_OK;
+}
+
+dsa3d_status check_backward_call(const dsa3d_desc* desc, const BackwardArgs& a,
+                                 const void* workspace, size_t workspace_bytes,
+                                 size_t scratch_limit, Geometry* gp) {
+  Geometry& g = *gp;
+  uint64_t rows, io_bytes, f32_bytes, off_bytes;
+  dsa3d_status st = check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes);
+  if (st != DSA3D_OK) return st;
+  if (!a.q || !a.k || !a.v || !a.offsets || !a.lse || !a.dout || !a.dq || !a.dk || !a.dv ||
+      !a.d_offsets)
+    return DSA3D_ERR_NULL_POINTER;
+  st = check_backward_range(g, rows);
+  if (st != DSA3D_OK) return st;
+  const size_t ws_need = backward_workspace_bytes(g);
+  if (scratch_limit > 0) {
+    if (ws_need > scratch_limit) return DSA3D_ERR_SCRATCH;
+  } else {
+    if (workspace == nullptr || workspace_bytes < ws_need) return DSA3D_ERR_WORKSPACE;
+    if (!aligned(workspace, 256)) return DSA3D_ERR_MISALIGNED;
+  }
+  if (!aligned(a.q, 16) || !aligned(a.k, 16) || !aligned(a.v, 16) || !aligned(a.dout, 16) ||
+      !aligned(a.dq, 16) || !aligned(a.dk, 16) || !aligned(a.dv, 16) ||
+      (a.out && !aligned(a.out, 16)) || !aligned(a.offsets, 4) || !aligned(a.lse, 4) ||
+      !aligned(a.d_offsets, 4))
+    return DSA3D_ERR_MISALIGNED;
+  // out (optional, not read) counts as an input: outputs and the workspace must avoid it
+  const Span in[] = {span_of(a.q, io_bytes),       span_of(a.k, io_bytes),
+                     span_of(a.v, io_bytes),       span_of(a.offsets, off_bytes),
+                     span_of(a.lse, rows * 4),     span_of(a.dout, io_bytes),
+                     span_of(a.out, a.out ? io_bytes : 0)};
+  const Span outs[] = {span_of(a.dq, f32_bytes), span_of(a.dk, f32_bytes),
+                       span_of(a.dv, f32_bytes), span_of(a.d_offsets, off_bytes)};
+  // the library's own scratch is a separate allocation: it overlaps nothing of the caller's
+  const Span sw = span_of(scratch_limit > 0 ? nullptr : workspace, scratch_limit > 0 ? 0 : ws_need);
+  for (int i = 0; i < 4; ++i) {
+    for (const Span& s : in)
+      if (overlaps(outs[i], s)) return DSA3D_ERR_ALIAS;
+    for (int j = i + 1; j < 4; ++j)
+      if (overlaps(outs[i], outs[j])) return DSA3D_ERR_ALIAS;
+    if (overlaps(outs[i], sw)) return DSA3D_ERR_ALIAS;
+  }
+  for (const Span& s : in)
+    if (overlaps(sw, s)) return DSA3D_ERR_ALIAS;
+  return DSA3D_OK;
+}
+
 }  // namespace dsa3d
 
 extern "C" {
@@ -96,6 +150,8 @@ const char* dsa3d_status_string(dsa3d_status s) {
       return "an output overlaps another argument";
     case DSA3D_ERR_DEVICE:
       return "HIP launch failed";
+    case DSA3D_ERR_SCRATCH:
+      return "problem needs more workspace than the library's fixed scratch buffer";
   }
   return "unknown status";
 }
@@ -126,19 +182,11 @@ dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k,
   return e == hipSuccess ? DSA3D_OK : DSA3D_ERR_DEVICE;
 }
 
-// The backward bins every (query row, point) pair by its trilinear cell; bin ranks and entry
-// slots are 32-bit, so rows * P and the number of cells must stay below 2^31.
-static dsa3d_status check_backward_range(const dsa3d::Geometry& g, uint64_t rows) {
-  const uint64_t cells = (uint64_t)(g.T + 1) * (g.H + 1) * (g.W + 1) * g.B * g.heads;
-  if (rows * (uint64_t)g.P >= (1ull << 31) || cells >= (1ull << 31)) return DSA3D_ERR_INVALID_SHAPE;
-  return DSA3D_OK;
-}
-
 size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc) {
   dsa3d::Geometry g;
   uint64_t rows, io_bytes, f32_bytes, off_bytes;
   if (check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes) != DSA3D_OK) return 0;
-  if (check_backward_range(g, rows) != DSA3D_OK) return 0;
+  if (dsa3d::check_backward_range(g, rows) != DSA3D_OK) return 0;
   return dsa3d::backward_workspace_bytes(g);
 }
 
@@ -148,38 +196,10 @@ dsa3d_status dsa3d_backward_timed(const dsa3d_desc* desc, const void* q, const v
                                   float* dv, float* d_offsets, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream,
                                   const hipEvent_t* events) {
+  const dsa3d::BackwardArgs a{q, k, v, offsets, out, lse, dout, dq, dk, dv, d_offsets};
   dsa3d::Geometry g;
-  uint64_t rows, io_bytes, f32_bytes, off_bytes;
-  dsa3d_status st = check_desc(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes);
+  const dsa3d_status st = dsa3d::check_backward_call(desc, a, workspace, workspace_bytes, 0, &g);
   if (st != DSA3D_OK) return st;
-  if (!q || !k || !v || !offsets || !lse || !dout || !dq || !dk || !dv || !d_offsets)
-    return DSA3D_ERR_NULL_POINTER;
-  st = check_backward_range(g, rows);
-  if (st != DSA3D_OK) return st;
-  const size_t ws_need = dsa3d::backward_workspace_bytes(g);
-  if (workspace == nullptr || workspace_bytes < ws_need) return DSA3D_ERR_WORKSPACE;
-  if (!aligned(workspace, 256)) return DSA3D_ERR_MISALIGNED;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dout, 16) ||
-      !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) || (out && !aligned(out, 16)) ||
-      !aligned(offsets, 4) || !aligned(lse, 4) || !aligned(d_offsets, 4))
-    return DSA3D_ERR_MISALIGNED;
-  // out (optional, not read) counts as an input: outputs and the workspace must avoid it
-  const Span in[] = {span_of(q, io_bytes),         span_of(k, io_bytes),
-                     span_of(v, io_bytes),         span_of(offsets, off_bytes),
-                     span_of(lse, rows * 4),       span_of(dout, io_bytes),
-                     span_of(out, out ? io_bytes : 0)};
-  const Span outs[] = {span_of(dq, f32_bytes), span_of(dk, f32_bytes), span_of(dv, f32_bytes),
-                       span_of(d_offsets, off_bytes)};
-  const Span sw = span_of(workspace, ws_need);
-  for (int a = 0; a < 4; ++a) {
-    for (const Span& s : in)
-      if (overlaps(outs[a], s)) return DSA3D_ERR_ALIAS;
-    for (int b = a + 1; b < 4; ++b)
-      if (overlaps(outs[a], outs[b])) return DSA3D_ERR_ALIAS;
-    if (overlaps(outs[a], sw)) return DSA3D_ERR_ALIAS;
-  }
-  for (const Span& s : in)
-    if (overlaps(sw, s)) return DSA3D_ERR_ALIAS;
   const hipError_t e = dsa3d::launch_backward(g, desc->dtype == DSA3D_BF16, q, k, v, nullptr,
                                               offsets, lse, dout, dq, dk, dv, d_offsets, nullptr,
                                               workspace, stream, events);
@@ -241,7 +261,7 @@ size_t dsa3d_pw_backward_workspace_size(const dsa3d_desc* desc) {
   uint64_t rows, io_bytes, f32_bytes, off_bytes, logit_bytes;
   if (check_pw(desc, &g, &rows, &io_bytes, &f32_bytes, &off_bytes, &logit_bytes) != DSA3D_OK)
     return 0;
-  if (check_backward_range(g, rows) != DSA3D_OK) return 0;
+  if (dsa3d::check_backward_range(g, rows) != DSA3D_OK) return 0;
   return dsa3d::backward_workspace_bytes(g);
 }
 
@@ -256,7 +276,7 @@ dsa3d_status dsa3d_pw_backward(const dsa3d_desc* desc, const float* logits, cons
   if (st != DSA3D_OK) return st;
   if (!logits || !v || !offsets || !lse || !dout || !dlogits || !dv || !d_offsets)
     return DSA3D_ERR_NULL_POINTER;
-  st = check_backward_range(g, rows);
+  st = dsa3d::check_backward_range(g, rows);
   if (st != DSA3D_OK) return st;
   const size_t ws_need = dsa3d::backward_workspace_bytes(g);
   if (workspace == nullptr || workspace_bytes < ws_need) return DSA3D_ERR_WORKSPACE;

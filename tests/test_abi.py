@@ -33,7 +33,7 @@ def test_library_exports_every_declared_function():
 
 def test_abi_version_and_status_strings():
     assert dsa.dsa3d_abi_version() == 1
-    for s in range(0, 8):
+    for s in range(0, 9):
         assert isinstance(dsa.status_string(s), str) and dsa.status_string(s)
     assert dsa.status_string(99) == "unknown status"
 
@@ -153,12 +153,38 @@ def test_backward_out_is_optional_but_checked_when_given():
     assert bwd_timed(d, out=names[8]) == B.DSA3D_ERR_ALIAS      # out == dk
 
 
+def noalloc(desc, **over):
+    names = BWD_NAMES[:-1]
+    args = dict(zip(names, ptrs(len(names))))
+    args.update(over)
+    return dsa.dsa3d_backward_noalloc(desc, *[args[n] for n in names], stream=0, check=False)
+
+
+def test_noalloc_backward_checks_before_touching_the_device():
+    """The no-allocation backward validates like dsa3d_backward (minus the workspace) and
+    rejects a problem whose workspace exceeds its fixed scratch, all on the host."""
+    d = good_desc()
+    assert noalloc(good_desc(kt=2)) == B.DSA3D_ERR_INVALID_SHAPE
+    assert noalloc(d, dq=None) == B.DSA3D_ERR_NULL_POINTER
+    assert noalloc(d, dk=ptrs(16)[15] + 4) == B.DSA3D_ERR_MISALIGNED
+    assert noalloc(d, dv=ptrs(1)[0]) == B.DSA3D_ERR_ALIAS            # dv == q
+    big = good_desc(T=16, H=64, W=64, heads=2, head_dim=64, kt=3, kh=3, kw=3)
+    assert dsa.dsa3d_backward_workspace_size(big) > B.DSA3D_NOALLOC_SCRATCH_BYTES
+    assert noalloc(big) == B.DSA3D_ERR_SCRATCH
+    fits = good_desc(T=8, H=32, W=32, heads=2, head_dim=64)
+    assert dsa.dsa3d_backward_workspace_size(fits) <= B.DSA3D_NOALLOC_SCRATCH_BYTES
+    src = open(os.path.join(INCLUDE, "dsa3d.h")).read()
+    assert re.search(r"DSA3D_NOALLOC_SCRATCH_BYTES \(128u << 20\)", src)
+    assert B.DSA3D_NOALLOC_SCRATCH_BYTES == 128 << 20
+
+
 def test_status_codes_match_the_header():
     src = open(os.path.join(INCLUDE, "dsa3d.h")).read()
     codes = dict((n, int(v)) for n, v in re.findall(r"\b(DSA3D_(?:OK|ERR_[A-Z_]+))\s*=\s*(\d+)", src))
     assert codes == {"DSA3D_OK": 0, "DSA3D_ERR_NULL_POINTER": 1, "DSA3D_ERR_INVALID_SHAPE": 2,
                      "DSA3D_ERR_UNSUPPORTED": 3, "DSA3D_ERR_MISALIGNED": 4,
-                     "DSA3D_ERR_WORKSPACE": 5, "DSA3D_ERR_DEVICE": 6, "DSA3D_ERR_ALIAS": 7}
+                     "DSA3D_ERR_WORKSPACE": 5, "DSA3D_ERR_DEVICE": 6, "DSA3D_ERR_ALIAS": 7,
+                     "DSA3D_ERR_SCRATCH": 8}
     for n, v in codes.items():
         assert getattr(B, n) == v, n
 
