@@ -122,8 +122,9 @@ def pmc_summary(workload, read_dir, write_dir, copyr_dir, copyw_dir, copy_mib):
                                                         / true_bytes, 4)},
            "kernels": {}}
     for k in reads:
-        # the operator's kernels only (not the copy, fills or the gather microbenchmark)
-        if k not in writes or not k.endswith("_kernel"):
+        # the operator's kernels only (not the copy, torch's own kernels or the gather
+        # microbenchmark)
+        if k not in writes or not k.endswith("_kernel") or "elementwise" in k:
             continue
         rd = mean([read_bytes(c) for c in reads[k]])
         req = mean([c["TCC_EA0_RDREQ_sum"] for c in reads[k]])

@@ -97,7 +97,7 @@ typedef struct {
 dsa3d_status dsa3d_forward(const dsa3d_desc* desc, const void* q, const void* k, const void* v,
                            const float* offsets, void* out, float* lse, hipStream_t stream);
 
-/* Bytes of device workspace dsa3d_backward needs for `desc`: about 56 bytes per
+/* Bytes of device workspace dsa3d_backward needs for `desc`: about 60 bytes per
  * (query row, point) pair plus 12 bytes per trilinear cell.  Returns 0 for a descriptor that
  * dsa3d_backward would reject. */
 size_t dsa3d_backward_workspace_size(const dsa3d_desc* desc);
@@ -134,9 +134,10 @@ dsa3d_status dsa3d_backward(const dsa3d_desc* desc, const void* q, const void* k
                             const void* dout, float* dq, float* dk, float* dv, float* d_offsets,
                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Phases of dsa3d_backward, in launch order: 0 the sweep over query rows (dq, per-point
- * records, bin counts), 1 the exclusive scan of the bin counts, 2 the pass over points
- * (d_offsets, binned dK/dV coefficients), 3 the dK/dV gather over voxels. */
+/* Phases of dsa3d_backward, in launch order: 0 the pass over the V corners of every query row
+ * (da_p, per-point records, bin counts and ranks), 1 the exclusive scan of the bin counts, 2 the
+ * pass over the K corners (alpha_p, dq, and once a row's Delta is known its d_offsets and
+ * binned dK/dV coefficients), 3 the dK/dV gather over voxels. */
 #define DSA3D_BACKWARD_PHASES 4
 
 /* dsa3d_backward with phase timing, for benchmarks and profilers.  `events` is NULL or

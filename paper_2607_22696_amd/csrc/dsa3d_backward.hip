@@ -33,11 +33,14 @@ namespace {
 
 using namespace dev;
 
-// Per-point record of the backward: the half that needs the K corners (alpha_p, A_p) and
-// the half that needs the V corners (da_p, B_p), each one 16-byte store.
-struct __align__(16) PointRec {
-  float alpha, ax, ay, az;   // K half
-  float dalpha, bx, by, bz;  // V half
+// Per-point records of the backward, in two arrays so that a pass that forms one half
+// writes whole lines: the half that needs the K corners (alpha_p, A_p) and the half that needs
+// the V corners (da_p, B_p).
+struct __align__(16) RecK {
+  float alpha, ax, ay, az;
+};
+struct __align__(16) RecV {
+  float dalpha, bx, by, bz;
 };
 
 // A point's contribution to dK/dV, stored in the bin of its cell.
@@ -48,7 +51,7 @@ struct Entry {
   float fx, fy, fz;  // fractional position inside the cell
 };
 
-static_assert(sizeof(PointRec) == 32 && sizeof(Entry) == 24, "record layout");
+static_assert(sizeof(RecK) == 16 && sizeof(RecV) == 16 && sizeof(Entry) == 24, "record layout");
 
 // Register budget of the sweep and gather kernels: at head_dim <= 64 (8 rows per wave) three
 // waves per SIMD (at most 168 VGPRs) measured faster than the compiler's own allocation; at
@@ -88,8 +91,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
     Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
     const float* __restrict__ logits, const float* __restrict__ offsets,
     const float* __restrict__ lse, const void* __restrict__ dout, float* __restrict__ dq,
-    PointRec* __restrict__ recs, float* __restrict__ delta_out, uint32_t* __restrict__ counts,
-    PencilOrder po) {
+    RecK* __restrict__ reck, RecV* __restrict__ recv, float* __restrict__ delta_out,
+    uint32_t* __restrict__ counts, PencilOrder po) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -225,9 +228,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
         }
       }
       if (own) {
-        float4* dst = reinterpret_cast<float4*>(recs + row * g.P + p0 + sub);
-        dst[0] = rec0;
-        dst[1] = rec1;
+        *reinterpret_cast<float4*>(reck + row * g.P + p0 + sub) = rec0;
+        *reinterpret_cast<float4*>(recv + row * g.P + p0 + sub) = rec1;
       }
     }
     if constexpr (!PW) {
@@ -247,25 +249,27 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
 //
 // The same work as the sweep in two passes over the points, one over the V corners and one
 // over the K corners, so that each pass keeps only one of the two tensors' rows in the L2s.
-// The V pass forms da_p = <dout, v_p> and B_p and counts the bins; after the scan, the K pass
-// forms alpha_p, A_p, dq and Delta, and once a row's Delta is known its lanes finish the
-// row's points: d_offsets and the point's entry in its bin (what the finalize pass does in
-// the one-sweep order).
+// The V pass forms da_p = <dout, v_p> and B_p and counts the bins, keeping each point's rank
+// in its bin; after the scan, the K pass forms alpha_p, A_p, dq and Delta, and once a row's
+// Delta is known its lanes finish the row's points: d_offsets and the point's entry, placed
+// at its bin's start + its rank (what the finalize pass does in the one-sweep order).
 
 // d_offsets of point p of a row and its entry in the bin of its cell, once the row's Delta is
 // known.  (t, i, j): the query token; n its index in the batch item; bh its (batch, head)
 // group.  dlogits (the predicted-weights variant, else null) receives alpha_p (da_p - Delta).
-__device__ inline void finish_point(const Geometry& g, const PointRec& r, float delta,
+//   The entry's slot is starts[cell] + rank (the point's rank in its bin, from the V pass).
+__device__ inline void finish_point(const Geometry& g, const RecK& rk, const RecV& rv, float delta,
                                     const float* __restrict__ o, int bh, int n, int t, int i, int j,
                                     int p, float* __restrict__ d, float* __restrict__ dlogit,
-                                    uint32_t* __restrict__ cursor, Entry* __restrict__ entries) {
+                                    const uint32_t* __restrict__ starts, uint32_t rank,
+                                    Entry* __restrict__ entries) {
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
-  const float dd = r.dalpha - delta;
+  const float dd = rv.dalpha - delta;
   const float sa = g.scale * dd;
-  d[0] = r.alpha * fmaf(sa, r.ax, r.bx);
-  d[1] = r.alpha * fmaf(sa, r.ay, r.by);
-  d[2] = r.alpha * fmaf(sa, r.az, r.bz);
-  if (dlogit != nullptr) *dlogit = r.alpha * dd;
+  d[0] = rk.alpha * fmaf(sa, rk.ax, rv.bx);
+  d[1] = rk.alpha * fmaf(sa, rk.ay, rv.by);
+  d[2] = rk.alpha * fmaf(sa, rk.az, rv.bz);
+  if (dlogit != nullptr) *dlogit = rk.alpha * dd;
   const int iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
   int x, y, z;
   float fx, fy, fz;
@@ -273,11 +277,11 @@ __device__ inline void finish_point(const Geometry& g, const PointRec& r, float 
   axis((float)(i + ih - rh), o[1], g.H, y, fy);
   axis((float)(t + it - rt), o[2], g.T, z, fz);
   if (!cell_inside(g, x, y, z)) return;
-  const uint32_t slot = atomicAdd(cursor + cell_index(g, bh, x, y, z), 1u);
+  const uint32_t slot = starts[cell_index(g, bh, x, y, z)] + rank;
   Entry e;
   e.n = (int32_t)n;
-  e.alpha = r.alpha;
-  e.sds = g.scale * r.alpha * dd;
+  e.alpha = rk.alpha;
+  e.sds = g.scale * rk.alpha * dd;
   e.fx = fx;
   e.fy = fy;
   e.fz = fz;
@@ -319,8 +323,8 @@ __device__ inline __attribute__((always_inline)) void weight_grad(const Point& p
 template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_kernel(
     Geometry g, const void* __restrict__ v, const float* __restrict__ offsets,
-    const void* __restrict__ dout, PointRec* __restrict__ recs, uint32_t* __restrict__ counts,
-    PencilOrder po) {
+    const void* __restrict__ dout, RecV* __restrict__ recv, uint32_t* __restrict__ counts,
+    uint32_t* __restrict__ ranks, PencilOrder po) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -352,9 +356,12 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
       Point mine;
       make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
       const bool own = p0 + sub < g.P;
-      if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))  // result unused: no wait
-        __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // the point's rank in its bin: the K pass puts its entry at bin start + rank (the
+      // returning atomic's latency is covered by the chunk's corner loads)
+      uint32_t rank = 0u;
+      if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))
+        rank = __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
+                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       pm = min(p0 + L + sub, g.P - 1);  // next chunk's offsets, in flight during this one
       ox = off[3 * pm];
       oy = off[3 * pm + 1];
@@ -384,7 +391,10 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
         for (int a = 0; a < 3; ++a) b3[a] = group_sum<L>(b3[a]);
         if (sub == kk) rec = make_float4(da, b3[0], b3[1], b3[2]);
       }
-      if (own) reinterpret_cast<float4*>(recs + row * g.P + p0 + sub)[1] = rec;
+      if (own) {
+        *reinterpret_cast<float4*>(recv + row * g.P + p0 + sub) = rec;
+        ranks[row * g.P + p0 + sub] = rank;
+      }
     }
   }
 }
@@ -396,8 +406,9 @@ template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k,
     const float* __restrict__ offsets, const float* __restrict__ lse, float* __restrict__ dq,
-    PointRec* __restrict__ recs, uint32_t* __restrict__ cursor, float* __restrict__ doff,
-    Entry* __restrict__ entries, PencilOrder po) {
+    RecK* __restrict__ reck, const RecV* __restrict__ recv, const uint32_t* __restrict__ starts,
+    const uint32_t* __restrict__ ranks, float* __restrict__ doff, Entry* __restrict__ entries,
+    PencilOrder po) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
   constexpr int VEC = LY::kVec;
@@ -424,7 +435,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
     const uint4 qr = load16(qb, row * LY::kRowBytes + lane_off);
     const float lse2 = lse[row] * kLog2e;
     const float* off = offsets + row * g.P * 3;
-    PointRec* rrow = recs + row * g.P;
+    RecK* krow = reck + row * g.P;
+    const RecV* vrow = recv + row * g.P;
     float ak[VEC], bk[VEC];
 #pragma unroll
     for (int x = 0; x < VEC; ++x) {
@@ -439,7 +451,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
       Point mine;
       make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
       const bool own = p0 + sub < g.P;
-      const float my_da = rrow[pm].dalpha;  // this lane's point's da_p (V pass)
+      const float my_da = vrow[pm].dalpha;  // this lane's point's da_p (V pass)
       pm = min(p0 + L + sub, g.P - 1);
       ox = off[3 * pm];
       oy = off[3 * pm + 1];
@@ -481,7 +493,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
         for (int a = 0; a < 3; ++a) a3[a] = group_sum<L>(a3[a]);
         if (sub == kk) rec = make_float4(alpha, a3[0], a3[1], a3[2]);
       }
-      if (own) reinterpret_cast<float4*>(rrow + p0 + sub)[0] = rec;
+      if (own) *reinterpret_cast<float4*>(krow + p0 + sub) = rec;
     }
     float* dqr = dq + row * D + sub * VEC;
 #pragma unroll
@@ -494,8 +506,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
     // wrote the K half of exactly these records above, and program order makes its own
     // stores visible to its loads)
     for (int p = sub; p < g.P; p += L)
-      finish_point(g, rrow[p], delta, off + 3 * p, bh, n, t, i, j, p, doff + (row * g.P + p) * 3,
-                   nullptr, cursor, entries);
+      finish_point(g, krow[p], vrow[p], delta, off + 3 * p, bh, n, t, i, j, p, doff + (row * g.P + p) * 3,
+                   nullptr, starts, ranks[row * g.P + p], entries);
   }
 }
 
@@ -596,7 +608,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply_kernel(const uint32_t
 
 // dlogits (the predicted-weights variant, else null) receives alpha_p (da_p - Delta).
 __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
-    Geometry g, const float* __restrict__ offsets, const PointRec* __restrict__ recs,
+    Geometry g, const float* __restrict__ offsets, const RecK* __restrict__ reck,
+    const RecV* __restrict__ recv,
     const float* __restrict__ delta, uint32_t* __restrict__ cursor, float* __restrict__ doff,
     float* __restrict__ dlogits, Entry* __restrict__ entries, int npoints) {
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
@@ -605,14 +618,15 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
        idx += gridDim.x * blockDim.x) {
     const unsigned row = idx / P;
     const unsigned p = idx - row * P;
-    const PointRec r = recs[idx];
-    const float dd = r.dalpha - delta[row];
+    const RecK rk = reck[idx];
+    const RecV rv = recv[idx];
+    const float dd = rv.dalpha - delta[row];
     float* d = doff + (size_t)idx * 3;
     const float sa = g.scale * dd;
-    d[0] = r.alpha * fmaf(sa, r.ax, r.bx);
-    d[1] = r.alpha * fmaf(sa, r.ay, r.by);
-    d[2] = r.alpha * fmaf(sa, r.az, r.bz);
-    if (dlogits != nullptr) dlogits[idx] = r.alpha * dd;
+    d[0] = rk.alpha * fmaf(sa, rk.ax, rv.bx);
+    d[1] = rk.alpha * fmaf(sa, rk.ay, rv.by);
+    d[2] = rk.alpha * fmaf(sa, rk.az, rv.bz);
+    if (dlogits != nullptr) dlogits[idx] = rk.alpha * dd;
     const unsigned tok = row / heads;
     const unsigned m = row - tok * heads;
     const unsigned b = tok / N;
@@ -632,8 +646,8 @@ __global__ __launch_bounds__(kBlockThreads) void bwd_finalize_kernel(
     const uint32_t slot = atomicAdd(cursor + cell_index(g, b * heads + m, x, y, z), 1u);
     Entry e;
     e.n = (int32_t)n;
-    e.alpha = r.alpha;
-    e.sds = g.scale * r.alpha * dd;
+    e.alpha = rk.alpha;
+    e.sds = g.scale * rk.alpha * dd;
     e.fx = fx;
     e.fy = fy;
     e.fz = fz;
@@ -1136,9 +1150,11 @@ struct Workspace {
   uint32_t* starts;   // [cells + 1]
   uint32_t* cursor;   // [cells]
   uint32_t* sums;     // [ceil(cells / kScanBlockItems)]
-  PointRec* recs;     // [rows * P], 16-byte aligned
+  RecK* reck;         // [rows * P]
+  RecV* recv;         // [rows * P]
   float* delta;       // [rows]
   Entry* entries;     // [rows * P]
+  uint32_t* ranks;    // [rows * P]: a point's rank in its bin (the split sweep's slots)
   size_t bytes;
 };
 
@@ -1161,9 +1177,11 @@ Workspace carve(const Geometry& g, void* base) {
   w.starts = reinterpret_cast<uint32_t*>(take((cells + 1) * 4));
   w.cursor = reinterpret_cast<uint32_t*>(take(cells * 4));
   w.sums = reinterpret_cast<uint32_t*>(take(nsums * 4));
-  w.recs = reinterpret_cast<PointRec*>(take(points * sizeof(PointRec)));
+  w.reck = reinterpret_cast<RecK*>(take(points * sizeof(RecK)));
+  w.recv = reinterpret_cast<RecV*>(take(points * sizeof(RecV)));
   w.delta = reinterpret_cast<float*>(take(rows * 4));
   w.entries = reinterpret_cast<Entry*>(take(points * sizeof(Entry)));
+  w.ranks = reinterpret_cast<uint32_t*>(take(points * 4));
   w.bytes = off;
   return w;
 }
@@ -1203,15 +1221,15 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   const bool split = !pw;
   if ((e = mark(0)) != hipSuccess) return e;
   if (split) {
-    void* a[] = {(void*)&g, (void*)&v, (void*)&off, (void*)&dout, (void*)&w.recs,
-                 (void*)&w.counts, (void*)&po};
+    void* a[] = {(void*)&g, (void*)&v, (void*)&off, (void*)&dout, (void*)&w.recv,
+                 (void*)&w.counts, (void*)&w.ranks, (void*)&po};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_vpass_kernel<D, BF16>), dim3(blocks),
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   } else {
     void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,       (void*)&v,
                  (void*)&logits, (void*)&off,  (void*)&lse,     (void*)&dout,
-                 (void*)&dq,   (void*)&w.recs, (void*)&w.delta, (void*)&w.counts,
+                 (void*)&dq,   (void*)&w.reck, (void*)&w.recv, (void*)&w.delta, (void*)&w.counts,
                  (void*)&po};
     const void* kern = pw ? reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, true>)
                           : reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, false>);
@@ -1237,15 +1255,15 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   }
   if ((e = mark(2)) != hipSuccess) return e;
   if (split) {
-    void* a[] = {(void*)&g,      (void*)&q,        (void*)&k,    (void*)&off,
-                 (void*)&lse,    (void*)&dq,       (void*)&w.recs, (void*)&w.cursor,
-                 (void*)&doff,   (void*)&w.entries, (void*)&po};
+    void* a[] = {(void*)&g,    (void*)&q,       (void*)&k,       (void*)&off,
+                 (void*)&lse,  (void*)&dq,      (void*)&w.reck,  (void*)&w.recv, (void*)&w.starts,
+                 (void*)&w.ranks, (void*)&doff, (void*)&w.entries, (void*)&po};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_kpass_kernel<D, BF16>), dim3(blocks),
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   } else {
     const int npoints = (int)points;
-    void* a[] = {(void*)&g,      (void*)&off,     (void*)&w.recs,    (void*)&w.delta,
+    void* a[] = {(void*)&g,      (void*)&off,     (void*)&w.reck,  (void*)&w.recv,  (void*)&w.delta,
                  (void*)&w.cursor, (void*)&doff, (void*)&dlogits, (void*)&w.entries,
                  (void*)&npoints};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_finalize_kernel), dim3(grid_for(points)),
@@ -1255,11 +1273,14 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   if ((e = mark(3)) != hipSuccess) return e;
   if constexpr (BF16) {
     constexpr int NW = gather_waves<D>();
-    // cells: 4 x 2 voxel blocks of a frame pair; pencils of about 32 x 32 voxels (measured
-    // at 64x68x120 / 64x34x60: 108.3 / 3.42 ms, against 108.8 / 3.68 for 16 x 16 voxels,
-    // 110.6 / 3.76 for 8 x 8 and 132.5 / 3.25 for whole frames)
+    // cells: 4 x 2 voxel blocks of a frame pair; pencils of about 16 x 16 voxels at head_dim
+    // 128 (two-wave workgroups) and 32 x 32 below (four-wave workgroups).  Measured at
+    // 64x68x120 (head_dim 128) / 64x34x60 (64): 108.8 / 3.68 ms for 16 x 16, 108.3 / 3.42
+    // for 32 x 32, 110.6 / 3.76 for 8 x 8, 132.5 / 3.25 for whole frames; at 64x68x120
+    // 32 x 32 pencils hit L2 on 31% of its requests against 58%, the same time only
+    // because the gather then reads past L2 at the ceiling of such misses.
     const PencilOrder go = plan_pencils(g.B * g.heads, (g.T + 1) / 2, (g.H + 1) / 2,
-                                        (g.W + 3) / 4, NW, 16, 8);
+                                        (g.W + 3) / 4, NW, D >= 128 ? 8 : 16, D >= 128 ? 4 : 8);
     const int gblocks = grid_blocks(go.vtiles);
     void* a[] = {(void*)&g,         (void*)&q,  (void*)&dout, (void*)&w.starts,
                  (void*)&w.entries, (void*)&dk, (void*)&dv,   (void*)&go};

@@ -197,8 +197,8 @@ def test_workspace_size_follows_the_documented_formula():
         cells = d.batch * d.heads * (d.frames + 1) * (d.height + 1) * (d.width + 1)
         ws = dsa.dsa3d_backward_workspace_size(d)
         assert ws % 256 == 0
-        lo = 56 * rows * P + 12 * cells + 4 * rows
-        assert lo <= ws <= lo + 8 * 256 + 4 * (cells // 4096 + 1) + 4
+        lo = 60 * rows * P + 12 * cells + 4 * rows
+        assert lo <= ws <= lo + 9 * 256 + 4 * (cells // 4096 + 1) + 4
     assert dsa.dsa3d_backward_workspace_size(good_desc(kt=2)) == 0
 
 
