@@ -48,12 +48,18 @@ FAMILY_SOURCES = {
 
 
 def kernel_source_hash(family: str = "dsa") -> str:
-    """Hash of the device sources of one kernel family."""
+    """Hash of the device sources of one kernel family, comments and layout left out (a
+    change of a comment does not make counters taken on the same code stale)."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for name in FAMILY_SOURCES[family]:
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+        with open(os.path.join(CSRC, name), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        text = " ".join(text.split())
+        h.update(name.encode() + b"\0" + text.encode())
     return h.hexdigest()[:16]
 
 

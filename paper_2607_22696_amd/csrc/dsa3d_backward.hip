@@ -7,25 +7,28 @@
 //   dK[x]         = sum over (query, point, corner c) landing on voxel x of scale ds_p w_c q
 //   dV[x]         = the same sum of alpha_p w_c dout
 //
-// Four launches, none with floating-point atomics:
-//  1. sweep (one L-lane group per query row, one pass over the points): loads the K and V
-//     corner rows, forms alpha_p and da_p, and keeps what depends on Delta factored:
-//       dq  = scale (sum_p alpha_p da_p k_p - Delta sum_p alpha_p k_p)
-//       d_offsets[p] = alpha_p (scale (da_p - Delta) A_p + B_p),
-//       A_p = sum_c dw_c/dpos <q, K_c>,  B_p = sum_c dw_c/dpos <dout, V_c>,
-//     so dq is final at the end of the sweep; (alpha_p, da_p, A_p, B_p) go to a 32-byte
-//     record per point.  Every point is also counted into the bin of its trilinear cell
-//     (the floor of its position) with an integer atomic whose result is not waited on.
-//  2. exclusive scan of the bin counts -> bin starts (and a copy used as fill cursors).
-//  3. finalize (one thread per point): d_offsets from A_p, B_p and the row's Delta; the
-//     point claims a slot of its bin from the cursor and writes its dK/dV coefficients
-//     (scale ds_p, alpha_p) and fractional position there, i.e. sorted by cell.
+// Four phases, none with floating-point atomics:
+//  1. V pass (one L-lane group per query row): loads the V corner rows of each point, forms
+//     da_p and B_p = sum_c dw_c/dpos <dout, V_c> (the V half of the point's record), and
+//     counts the point into the bin of its trilinear cell (the floor of its position) with
+//     an integer atomic whose result, the point's rank in the bin, is kept.
+//  2. exclusive scan of the bin counts -> bin starts.
+//  3. K pass (one L-lane group per query row): loads the K corner rows, forms alpha_p from the
+//     logit and the forward's LSE, A_p = sum_c dw_c/dpos <q, K_c>, Delta = sum_p alpha_p da_p
+//     and dq, keeping the Delta-dependent part factored until the row's last point,
+//       dq = scale (sum_p alpha_p da_p k_p - Delta sum_p alpha_p k_p);
+//     then the row's lanes finish its points: d_offsets[p] = alpha_p (scale (da_p - Delta) A_p
+//     + B_p), and the point's dK/dV coefficients (scale ds_p, alpha_p) and fractional position
+//     go to slot bin start + rank, i.e. sorted by cell.
 //  4. gather: a voxel is corner c of exactly the points whose cell is voxel - c, so a block
 //     of voxels reads the bins of the cells around it, a few runs of adjacent bins, and
 //     stores the dK and dV rows of its voxels once.  bf16: one wave per 4 x 2 x 2 block, the
 //     sums as matrix products (weights x q / dout rows) on the matrix cores; fp32: one
 //     L-lane group per 2 x 2 block of a frame, w_c * coefficient * q and * dout accumulated
 //     in registers.
+// The predicted-weights variant reads no K: one sweep (phase 1 with the given logits, the
+// bin counts' ranks not kept) and a finalize of one thread per point that claims its slot
+// from a fill cursor take phases 1 and 3.
 #include "dsa3d_device.h"
 
 namespace dsa3d {

@@ -155,3 +155,17 @@ def test_pmc_summary_counts_read_requests_by_size(tmp_path, monkeypatch):
     assert kr["atomics_l2"] == 7 and kr["atomics_past_l2"] == 3
     assert kr["read_requests_of_known_size"] == 1.0
     assert doc["copy_check"] == {"mib": 1, "read_bytes_per_byte": 1.0, "write_bytes_per_byte": 1.0}
+
+
+def test_kernel_source_hash_ignores_comments_but_not_code(tmp_path, monkeypatch):
+    import shutil
+    for name in bench.FAMILY_SOURCES["win"]:
+        shutil.copy(os.path.join(bench.CSRC, name), tmp_path / name)
+    monkeypatch.setattr(bench, "CSRC", str(tmp_path))
+    h0 = bench.kernel_source_hash("win")
+    src = tmp_path / bench.FAMILY_SOURCES["win"][0]
+    text = src.read_text()
+    src.write_text("// a new comment\n/* and a block\n   comment */\n" + text.replace("\n", "  \n", 3))
+    assert bench.kernel_source_hash("win") == h0
+    src.write_text(text + "\nstatic int added_code = 1;\n")
+    assert bench.kernel_source_hash("win") != h0
