@@ -257,38 +257,72 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
 // Delta is known its lanes finish the row's points: d_offsets and the point's entry, placed
 // at its bin's start + its rank (what the finalize pass does in the one-sweep order).
 
-// d_offsets of point p of a row and its entry in the bin of its cell, once the row's Delta is
-// known.  (t, i, j): the query token; n its index in the batch item; bh its (batch, head)
-// group.  dlogits (the predicted-weights variant, else null) receives alpha_p (da_p - Delta).
-//   The entry's slot is starts[cell] + rank (the point's rank in its bin, from the V pass).
-__device__ inline void finish_point(const Geometry& g, const RecK& rk, const RecV& rv, float delta,
-                                    const float* __restrict__ o, int bh, int n, int t, int i, int j,
-                                    int p, float* __restrict__ d, float* __restrict__ dlogit,
-                                    const uint32_t* __restrict__ starts, uint32_t rank,
-                                    Entry* __restrict__ entries) {
+// The row's points once its Delta is known, kFinish per lane at a time so that their loads
+// (record halves, offsets, ranks) and then their bin-start lookups are in flight together:
+// d_offsets of each point and its entry in the bin of its cell, at slot starts[cell] + rank
+// (the point's rank in its bin, from the V pass).  Lane `sub` takes points sub, sub + L, ...:
+// it wrote the K half of exactly these records, and program order makes its own stores
+// visible to its loads.  (t, i, j): the query token; n its index in the batch item; bh its
+// (batch, head) group; row its query row.
+constexpr int kFinish = 4;
+
+template <int L>
+__device__ inline __attribute__((always_inline)) void finish_row(
+    const Geometry& g, const RecK* __restrict__ krow, const RecV* __restrict__ vrow,
+    const float* __restrict__ off, const uint32_t* __restrict__ rrow, float delta, int bh, int n,
+    int t, int i, int j, int sub, float* __restrict__ drow, const uint32_t* __restrict__ starts,
+    Entry* __restrict__ entries) {
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
-  const float dd = rv.dalpha - delta;
-  const float sa = g.scale * dd;
-  d[0] = rk.alpha * fmaf(sa, rk.ax, rv.bx);
-  d[1] = rk.alpha * fmaf(sa, rk.ay, rv.by);
-  d[2] = rk.alpha * fmaf(sa, rk.az, rv.bz);
-  if (dlogit != nullptr) *dlogit = rk.alpha * dd;
-  const int iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
-  int x, y, z;
-  float fx, fy, fz;
-  axis((float)(j + iw - rw), o[0], g.W, x, fx);
-  axis((float)(i + ih - rh), o[1], g.H, y, fy);
-  axis((float)(t + it - rt), o[2], g.T, z, fz);
-  if (!cell_inside(g, x, y, z)) return;
-  const uint32_t slot = starts[cell_index(g, bh, x, y, z)] + rank;
-  Entry e;
-  e.n = (int32_t)n;
-  e.alpha = rk.alpha;
-  e.sds = g.scale * rk.alpha * dd;
-  e.fx = fx;
-  e.fy = fy;
-  e.fz = fz;
-  entries[slot] = e;
+  for (int p0 = sub; p0 < g.P; p0 += kFinish * L) {
+    RecK rk[kFinish];
+    RecV rv[kFinish];
+    float o[kFinish][3];
+    uint32_t rank[kFinish];
+#pragma unroll
+    for (int u = 0; u < kFinish; ++u) {
+      const int p = min(p0 + u * L, g.P - 1);  // past the row's end: a repeat, not stored
+      rk[u] = krow[p];
+      rv[u] = vrow[p];
+      o[u][0] = off[3 * p];
+      o[u][1] = off[3 * p + 1];
+      o[u][2] = off[3 * p + 2];
+      rank[u] = rrow[p];
+    }
+    int cx[kFinish], cy[kFinish], cz[kFinish];
+    float fx[kFinish], fy[kFinish], fz[kFinish];
+    uint32_t slot[kFinish];
+#pragma unroll
+    for (int u = 0; u < kFinish; ++u) {
+      const int p = min(p0 + u * L, g.P - 1);
+      const int iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
+      axis((float)(j + iw - rw), o[u][0], g.W, cx[u], fx[u]);
+      axis((float)(i + ih - rh), o[u][1], g.H, cy[u], fy[u]);
+      axis((float)(t + it - rt), o[u][2], g.T, cz[u], fz[u]);
+      slot[u] = 0xffffffffu;
+      if (cell_inside(g, cx[u], cy[u], cz[u]))
+        slot[u] = starts[cell_index(g, bh, cx[u], cy[u], cz[u])] + rank[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kFinish; ++u) {
+      const int p = p0 + u * L;
+      if (p >= g.P) break;
+      const float dd = rv[u].dalpha - delta;
+      const float sa = g.scale * dd;
+      float* d = drow + 3 * p;
+      d[0] = rk[u].alpha * fmaf(sa, rk[u].ax, rv[u].bx);
+      d[1] = rk[u].alpha * fmaf(sa, rk[u].ay, rv[u].by);
+      d[2] = rk[u].alpha * fmaf(sa, rk[u].az, rv[u].bz);
+      if (slot[u] == 0xffffffffu) continue;
+      Entry e;
+      e.n = (int32_t)n;
+      e.alpha = rk[u].alpha;
+      e.sds = g.scale * rk[u].alpha * dd;
+      e.fx = fx[u];
+      e.fy = fy[u];
+      e.fz = fz[u];
+      entries[slot[u]] = e;
+    }
+  }
 }
 
 // Point setup shared by the two passes: the row's lanes fetch point `kk` of the chunk from the
@@ -404,7 +438,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
 
 // K pass: alpha_p from the logit and the forward's LSE, A_p = sum_c dw_c/dpos <q, K_c> into the
 // K half of the record, Delta = sum_p alpha_p da_p and dq; then, with Delta known, the row's
-// lanes finish its points (finish_point).  Needs the V pass's records and the bin starts.
+// lanes finish its points (finish_row).  Needs the V pass's records and the bin starts.
 template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k,
@@ -505,12 +539,9 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
           make_float4(g.scale * fmaf(-delta, bk[x], ak[x]), g.scale * fmaf(-delta, bk[x + 1], ak[x + 1]),
                       g.scale * fmaf(-delta, bk[x + 2], ak[x + 2]),
                       g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
-    // Delta is known: finish the row's points (lane sub takes points sub, sub + L, ...; it
-    // wrote the K half of exactly these records above, and program order makes its own
-    // stores visible to its loads)
-    for (int p = sub; p < g.P; p += L)
-      finish_point(g, krow[p], vrow[p], delta, off + 3 * p, bh, n, t, i, j, p, doff + (row * g.P + p) * 3,
-                   nullptr, starts, ranks[row * g.P + p], entries);
+    // Delta is known: finish the row's points
+    finish_row<L>(g, krow, vrow, off, ranks + row * g.P, delta, bh, n, t, i, j, sub,
+                  doff + row * g.P * 3, starts, entries);
   }
 }
 
