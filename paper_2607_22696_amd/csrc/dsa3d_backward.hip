@@ -870,9 +870,13 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int kGB = 32;  // entries per batch: the products' K
 
-// waves per workgroup: the LDS of a wave grows with head_dim
+// Waves per workgroup.  The LDS of a wave grows with head_dim, and at head_dim 128 (20.4 KB
+// per wave) LDS bounds the waves per compute unit: one-wave workgroups let seven share it
+// against six in two-wave workgroups, and the gather waits on its rows' loads, so the extra
+// wave's loads in flight took it from 102 to 87 ms at 64x68x120 with a 3x5x5 kernel (210 to
+// 180 ms with 3x7x7).  At head_dim 64 (12.7 KB) registers bound it at three per SIMD first.
 template <int D>
-constexpr int gather_waves() { return D <= 64 ? 4 : 2; }
+constexpr int gather_waves() { return D <= 64 ? 4 : 1; }
 
 template <int D, bool PW>
 struct GatherLds {
@@ -1308,7 +1312,7 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
   if constexpr (BF16) {
     constexpr int NW = gather_waves<D>();
     // cells: 4 x 2 voxel blocks of a frame pair; pencils of about 16 x 16 voxels at head_dim
-    // 128 (two-wave workgroups) and 32 x 32 below (four-wave workgroups).  Measured at
+    // 128 and 32 x 32 below.  Measured (with two-wave workgroups at head_dim 128) at
     // 64x68x120 (head_dim 128) / 64x34x60 (64): 108.8 / 3.68 ms for 16 x 16, 108.3 / 3.42
     // for 32 x 32, 110.6 / 3.76 for 8 x 8, 132.5 / 3.25 for whole frames; at 64x68x120
     // 32 x 32 pencils hit L2 on 31% of its requests against 58%, the same time only
