@@ -870,11 +870,13 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int kGB = 32;  // entries per batch: the products' K
 
-// Waves per workgroup.  The LDS of a wave grows with head_dim, and at head_dim 128 (20.4 KB
-// per wave) LDS bounds the waves per compute unit: one-wave workgroups let seven share it
-// against six in two-wave workgroups, and the gather waits on its rows' loads, so the extra
-// wave's loads in flight took it from 102 to 87 ms at 64x68x120 with a 3x5x5 kernel (210 to
-// 180 ms with 3x7x7).  At head_dim 64 (12.7 KB) registers bound it at three per SIMD first.
+// Waves per workgroup.  The LDS of a wave grows with head_dim, and at head_dim 128 LDS and
+// registers both bound the waves per compute unit.  The gather waits on its rows' loads, so
+// waves are worth their LDS: one-wave workgroups of 20 KB (the rows and A^T only) let eight
+// waves share a compute unit, against six for two-wave workgroups that also kept the run
+// table and the batch's tokens in LDS (20.4 KB per wave): 102 -> 81 ms at 64x68x120 with a
+// 3x5x5 kernel, 210 -> 152 ms with 3x7x7.  At head_dim 64 (12 KB) registers bound it at
+// three waves per SIMD first.
 template <int D>
 constexpr int gather_waves() { return D <= 64 ? 4 : 1; }
 
@@ -883,10 +885,10 @@ struct GatherLds {
   uint16_t q[PW ? 8 : kGB * D];  // the batch's rows, 16-byte chunks permuted per row
   uint16_t g[kGB * D];
   uint16_t a[PW ? 2 : 4][kGB * 16];  // A^T: (dV hi, dV lo[, dK hi, dK lo]), 32 rows of 16 bf16
-  int tok[kGB];     // the batch's query tokens, read by the lanes that copy their rows
-  uint4 run[9][2];  // cell starts x0-1 .. x0+3 and the end, of the non-empty runs
-  int rc[9];        // their cell row / plane: (y - y0 + 1) + 3 (z - z0 + 1)
 };
+// The rows and A^T only (the run table stays in the registers of the lanes that read it, the
+// tokens are broadcast with ds_bpermute): 20 KB per wave at head_dim 128, so that eight waves
+// fit in a compute unit's 160 KB.
 
 // The 16-byte chunks of row e are permuted by XOR with 2 s(e), so that each half-wave of a
 // transposing read (for groups G = 0, 1 or 2, 3: rows 8 G + {0..3}, or 8 G + {4..7}, 32 bytes
@@ -964,7 +966,8 @@ __device__ inline void weight_rows(float c, float fx, float fy, float fz, int rc
 // m1 .. m4 (cell x0 - 1 starts at or before u); u >= end once the runs are exhausted.
 struct GatherPos {
   uint32_t u, end, m1, m2, m3, m4;
-  int rc, r;
+  int rc;         // the run's cell row / plane: (y - y0 + 1) + 3 (z - z0 + 1)
+  uint64_t left;  // lanes holding the runs after this one
 };
 
 // This lane's 16 bytes of an entry: lanes 0-31 read (n, alpha, sds, fx), lanes 32-63 read
@@ -1018,25 +1021,20 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
         has = c[0] < c[5];
       }
     }
+    // lane r < 9 keeps its run's bounds in c[]; the wave reads the runs in lane order with
+    // readlane, `left` marking the lanes whose runs are still ahead
     const uint64_t hm = __builtin_amdgcn_ballot_w64(has);
-    const int nruns = __popcll(hm);
-    if (has) {
-      const int at = __popcll(hm & ((1ull << lane) - 1ull));
-      L.run[at][0] = make_uint4(c[0], c[1], c[2], c[3]);
-      L.run[at][1] = make_uint4(c[4], c[5], 0u, 0u);
-      L.rc[at] = lane;
-    }
-    auto load_run = [&](GatherPos& d, int r) {
-      d.r = r;
-      if (r < nruns) {
-        const uint4 t0 = L.run[r][0], t1 = L.run[r][1];
-        d.u = __builtin_amdgcn_readfirstlane(t0.x);
-        d.m1 = __builtin_amdgcn_readfirstlane(t0.y);
-        d.m2 = __builtin_amdgcn_readfirstlane(t0.z);
-        d.m3 = __builtin_amdgcn_readfirstlane(t0.w);
-        d.m4 = __builtin_amdgcn_readfirstlane(t1.x);
-        d.end = __builtin_amdgcn_readfirstlane(t1.y);
-        d.rc = __builtin_amdgcn_readfirstlane(L.rc[r]);
+    auto next_run = [&](GatherPos& d) {
+      if (d.left != 0ull) {
+        const int lr = __builtin_amdgcn_readfirstlane(__builtin_ctzll(d.left));
+        d.left &= d.left - 1ull;
+        d.u = __builtin_amdgcn_readlane(c[0], lr);
+        d.m1 = __builtin_amdgcn_readlane(c[1], lr);
+        d.m2 = __builtin_amdgcn_readlane(c[2], lr);
+        d.m3 = __builtin_amdgcn_readlane(c[3], lr);
+        d.m4 = __builtin_amdgcn_readlane(c[4], lr);
+        d.end = __builtin_amdgcn_readlane(c[5], lr);
+        d.rc = lr;
       } else {
         d.u = d.end = d.m1 = d.m2 = d.m3 = d.m4 = 0u;
         d.rc = 0;
@@ -1044,7 +1042,7 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
     };
     auto advance = [&](GatherPos& d) {
       d.u += kGB;
-      if (d.u >= d.end) load_run(d, d.r + 1);
+      if (d.u >= d.end) next_run(d);
     };
     // this lane's part of its entry (clamped to the run; the coefficient is zeroed outside it)
     auto fetch = [&](const GatherPos& d, GatherEntry& en) {
@@ -1080,11 +1078,11 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
     bool part = false;  // the batch ends inside: its rows past the end are zeroed in LDS
     auto issue_rows = [&](const GatherPos& d, const GatherEntry& en) {
       part = d.end - d.u < (uint32_t)kGB;
-      if (lane < kGB) L.tok[lane] = (int)en.raw.x;  // lanes 0-31 hold n
 #pragma unroll
       for (int t = 0; t < NI; ++t) {
         const int e = lane / LPR + RPI * t;
-        const uint32_t n = (uint32_t)L.tok[e];  // one dword per row, read by its LPR lanes
+        // entry e's token, from lane e (lanes 0-31 hold n), for the LPR lanes of its row
+        const uint32_t n = (uint32_t)__builtin_amdgcn_ds_bpermute(e << 2, (int)en.raw.x);
         const uint64_t o = (uint64_t)n * tok_bytes;
         if (d.u + e < d.end) {  // rows past the run's end are not loaded
           if constexpr (!PW) rq[t] = *reinterpret_cast<const uint4*>(qh + o);
@@ -1118,7 +1116,8 @@ void bwd_gather_mfma_kernel(Geometry g, const void* __restrict__ q, const void* 
     // i + 1, take batch i's products, then form batch i + 1's weights (p0, p1, p2: batches i,
     // i + 1, i + 2).
     GatherPos p0, p1, p2;
-    load_run(p0, 0);
+    p0.left = hm;
+    next_run(p0);
     if (p0.u < p0.end) {
       GatherEntry e1, e2;
       {
