@@ -286,6 +286,36 @@ __device__ inline __attribute__((always_inline)) void load_shared_corners(
   }
 }
 
+// The same with the owner's point read from its LDS slot (`at`: corner indices, weights, then
+// (window flag, cell x, y, z)) instead of from its registers.
+template <int ROW_BYTES, bool KV>
+__device__ inline __attribute__((always_inline)) void load_stashed_corners(
+    const Geometry& g, const RowWindow& win, const char* kb, const char* vb, int b, int m,
+    int lane_off, const int4* at, const int* vidx, uint4* kr, uint4* vr) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    if constexpr (KV) kr[c] = buffer_row(win.k, vidx[c], lane_off);
+    vr[c] = buffer_row(win.v, vidx[c], lane_off);
+  }
+  const int4 cell = at[4];
+  const bool slow = cell.x != 0;
+  if (__builtin_amdgcn_ballot_w64(slow)) {
+    if (slow) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const int x = cell.y + (c & 1), y = cell.z + ((c >> 1) & 1), z = cell.w + (c >> 2);
+        const bool inside = (unsigned)x < (unsigned)g.W && (unsigned)y < (unsigned)g.H &&
+                            (unsigned)z < (unsigned)g.T;
+        if (inside && (unsigned)(z - win.t0) >= (unsigned)win.frames) {
+          const int64_t row = ((((int64_t)b * g.T + z) * g.H + y) * g.W + x) * g.heads + m;
+          if constexpr (KV) kr[c] = load16(kb, row * ROW_BYTES + lane_off);
+          vr[c] = load16(vb, row * ROW_BYTES + lane_off);
+        }
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------- launch shape
 
 constexpr int kMaxBlocks = 1 << 22;  // grid cap; larger problems loop over tiles
