@@ -457,6 +457,13 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
   const int HW = g.H * g.W;
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const int khw = g.kh * g.kw;
+  // The point each lane formed for the current chunk, read back by its row's lanes (a row's
+  // lanes are one wave, whose LDS accesses complete in order): corner indices, weights, the
+  // magnitudes of the weights' position derivatives (the products of two axis weights),
+  // window flag and cell, and the point's da_p.  The owner forms them once instead of every
+  // lane of the row rebuilding them, which the VALU-bound point loop feels.
+  __shared__ int4 pts[kBlockThreads][9];
+  int4* const mine_at = pts[threadIdx.x];
 
   for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
     PencilTile tl;
@@ -485,10 +492,30 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
     float ox = off[3 * pm], oy = off[3 * pm + 1], oz = off[3 * pm + 2];
     for (int p0 = 0; p0 < g.P; p0 += L) {
       const int it = pm / khw, ih = (pm - it * khw) / g.kw, iw = pm - it * khw - ih * g.kw;
-      Point mine;
-      make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
+      {
+        Point mine;
+        make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
+        const float my_da = vrow[pm].dalpha;  // this lane's point's da_p (V pass)
+        const float* ax = mine.ax;
+        const float* ay = mine.ay;
+        const float* az = mine.az;
+        mine_at[0] = make_int4(mine.vidx[0], mine.vidx[1], mine.vidx[2], mine.vidx[3]);
+        mine_at[1] = make_int4(mine.vidx[4], mine.vidx[5], mine.vidx[6], mine.vidx[7]);
+        mine_at[2] = make_int4(__float_as_int(mine.w[0]), __float_as_int(mine.w[1]),
+                               __float_as_int(mine.w[2]), __float_as_int(mine.w[3]));
+        mine_at[3] = make_int4(__float_as_int(mine.w[4]), __float_as_int(mine.w[5]),
+                               __float_as_int(mine.w[6]), __float_as_int(mine.w[7]));
+        // |dw_c/dx| = ay az, |dw_c/dy| = ax az, |dw_c/dz| = ax ay, by the corner's other two bits
+        mine_at[4] = make_int4(__float_as_int(ay[0] * az[0]), __float_as_int(ay[1] * az[0]),
+                               __float_as_int(ay[0] * az[1]), __float_as_int(ay[1] * az[1]));
+        mine_at[5] = make_int4(__float_as_int(ax[0] * az[0]), __float_as_int(ax[1] * az[0]),
+                               __float_as_int(ax[0] * az[1]), __float_as_int(ax[1] * az[1]));
+        mine_at[6] = make_int4(__float_as_int(ax[0] * ay[0]), __float_as_int(ax[1] * ay[0]),
+                               __float_as_int(ax[0] * ay[1]), __float_as_int(ax[1] * ay[1]));
+        mine_at[7] = make_int4((int)mine.slow, mine.cx, mine.cy, mine.cz);
+        mine_at[8] = make_int4(__float_as_int(my_da), 0, 0, 0);
+      }
       const bool own = p0 + sub < g.P;
-      const float my_da = vrow[pm].dalpha;  // this lane's point's da_p (V pass)
       pm = min(p0 + L + sub, g.P - 1);
       ox = off[3 * pm];
       oy = off[3 * pm + 1];
@@ -496,29 +523,47 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_k
       const int nk = min(L, g.P - p0);
       float4 rec = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       for (int kk = 0; kk < nk; ++kk) {
-        const int src = (grp * L + kk) << 2;
-        Point pt;
-        fetch_point(mine, src, pt);
+        const int4* at = pts[wave * 64 + grp * L + kk];
+        int vidx[8];
+        {
+          const int4 i0 = at[0], i1 = at[1];
+          vidx[0] = i0.x; vidx[1] = i0.y; vidx[2] = i0.z; vidx[3] = i0.w;
+          vidx[4] = i1.x; vidx[5] = i1.y; vidx[6] = i1.z; vidx[7] = i1.w;
+        }
         uint4 kr[8];
-        load_shared_corners<LY::kRowBytes, false>(g, win, kb, kb, b, m, lane_off, mine, src,
-                                                  pt.vidx, nullptr, kr);
+        load_stashed_corners<LY::kRowBytes, false>(g, win, kb, kb, b, m, lane_off, at + 7, vidx,
+                                                   nullptr, kr);
+        float w[8], gx[4], gy[4], gz[4];
+        {
+          const int4 w0 = at[2], w1 = at[3], x4 = at[4], y4 = at[5], z4 = at[6];
+          w[0] = __int_as_float(w0.x); w[1] = __int_as_float(w0.y);
+          w[2] = __int_as_float(w0.z); w[3] = __int_as_float(w0.w);
+          w[4] = __int_as_float(w1.x); w[5] = __int_as_float(w1.y);
+          w[6] = __int_as_float(w1.z); w[7] = __int_as_float(w1.w);
+          gx[0] = __int_as_float(x4.x); gx[1] = __int_as_float(x4.y);
+          gx[2] = __int_as_float(x4.z); gx[3] = __int_as_float(x4.w);
+          gy[0] = __int_as_float(y4.x); gy[1] = __int_as_float(y4.y);
+          gy[2] = __int_as_float(y4.z); gy[3] = __int_as_float(y4.w);
+          gz[0] = __int_as_float(z4.x); gz[1] = __int_as_float(z4.y);
+          gz[2] = __int_as_float(z4.z); gz[3] = __int_as_float(z4.w);
+        }
         float sp = 0.0f, a3[3] = {0.0f, 0.0f, 0.0f};
         float kp[VEC];
 #pragma unroll
         for (int x = 0; x < VEC; ++x) kp[x] = 0.0f;
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
+          const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
           const float qk = chunk_dot<BF16>(qr, kr[c]);
-          float wx, wy, wz;
-          weight_grad(pt, c, wx, wy, wz);
-          sp = fmaf(pt.w[c], qk, sp);
-          a3[0] = fmaf(wx, qk, a3[0]);
-          a3[1] = fmaf(wy, qk, a3[1]);
-          a3[2] = fmaf(wz, qk, a3[2]);
-          chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
+          sp = fmaf(w[c], qk, sp);
+          // dw_c/dpos: + for the upper corner of an axis, - for the lower
+          a3[0] = fmaf(cx ? gx[c >> 1] : -gx[c >> 1], qk, a3[0]);
+          a3[1] = fmaf(cy ? gy[cx + 2 * cz] : -gy[cx + 2 * cz], qk, a3[1]);
+          a3[2] = fmaf(cz ? gz[c & 3] : -gz[c & 3], qk, a3[2]);
+          chunk_axpy<BF16>(kp, w[c], kr[c]);
         }
         const float alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
-        const float da = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(my_da)));
+        const float da = __int_as_float(at[8].x);
         delta = fmaf(alpha, da, delta);
         const float ada = alpha * da;
 #pragma unroll

@@ -286,18 +286,18 @@ __device__ inline __attribute__((always_inline)) void load_shared_corners(
   }
 }
 
-// The same with the owner's point read from its LDS slot (`at`: corner indices, weights, then
-// (window flag, cell x, y, z)) instead of from its registers.
+// The same with the owner's point read from its LDS slot instead of from its registers:
+// `cell` = (window flag, cell x, y, z) of that point, `cell_at` its place in the slot.
 template <int ROW_BYTES, bool KV>
 __device__ inline __attribute__((always_inline)) void load_stashed_corners(
     const Geometry& g, const RowWindow& win, const char* kb, const char* vb, int b, int m,
-    int lane_off, const int4* at, const int* vidx, uint4* kr, uint4* vr) {
+    int lane_off, const int4* cell_at, const int* vidx, uint4* kr, uint4* vr) {
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
     if constexpr (KV) kr[c] = buffer_row(win.k, vidx[c], lane_off);
     vr[c] = buffer_row(win.v, vidx[c], lane_off);
   }
-  const int4 cell = at[4];
+  const int4 cell = *cell_at;
   const bool slow = cell.x != 0;
   if (__builtin_amdgcn_ballot_w64(slow)) {
     if (slow) {

@@ -109,12 +109,12 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
         uint4 vr[8];
         float s2;
         if constexpr (PW) {
-          load_stashed_corners<LY::kRowBytes, false>(g, win, kb, vb, b, m, lane_off, at,
+          load_stashed_corners<LY::kRowBytes, false>(g, win, kb, vb, b, m, lane_off, at + 4,
                                                      pt.vidx, nullptr, vr);
           s2 = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mylog2)));
         } else {
           uint4 kr[8];
-          load_stashed_corners<LY::kRowBytes, true>(g, win, kb, vb, b, m, lane_off, at,
+          load_stashed_corners<LY::kRowBytes, true>(g, win, kb, vb, b, m, lane_off, at + 4,
                                                     pt.vidx, kr, vr);
           float sp = 0.0f;
 #pragma unroll
