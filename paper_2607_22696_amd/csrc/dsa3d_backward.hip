@@ -372,6 +372,15 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
   const int HW = g.H * g.W;
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
   const int khw = g.kh * g.kw;
+  // At 16 lanes per row the point each lane formed for the current chunk is read back by its
+  // row's lanes from LDS (a row's lanes are one wave, whose LDS accesses complete in order):
+  // corner indices, weights, the magnitudes of the weights' position derivatives, window flag
+  // and cell (as in the K pass).  At 8 lanes per row (a read then serves 8 rows) the lanes
+  // fetch indices and fractions with ds_bpermute and rebuild the rest, which measured faster
+  // there (2.98 against 3.10 ms at 64x34x60; 88.7 against 87.2 ms at 64x68x120, head_dim 128).
+  constexpr bool kSlots = L >= 16;
+  __shared__ int4 pts[kSlots ? kBlockThreads : 1][8];
+  int4* const mine_at = pts[kSlots ? threadIdx.x : 0];
 
   for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
     PencilTile tl;
@@ -392,6 +401,24 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
       const int it = pm / khw, ih = (pm - it * khw) / g.kw, iw = pm - it * khw - ih * g.kw;
       Point mine;
       make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
+      if constexpr (kSlots) {
+        const float* ax = mine.ax;
+        const float* ay = mine.ay;
+        const float* az = mine.az;
+        mine_at[0] = make_int4(mine.vidx[0], mine.vidx[1], mine.vidx[2], mine.vidx[3]);
+        mine_at[1] = make_int4(mine.vidx[4], mine.vidx[5], mine.vidx[6], mine.vidx[7]);
+        mine_at[2] = make_int4(__float_as_int(mine.w[0]), __float_as_int(mine.w[1]),
+                               __float_as_int(mine.w[2]), __float_as_int(mine.w[3]));
+        mine_at[3] = make_int4(__float_as_int(mine.w[4]), __float_as_int(mine.w[5]),
+                               __float_as_int(mine.w[6]), __float_as_int(mine.w[7]));
+        mine_at[4] = make_int4(__float_as_int(ay[0] * az[0]), __float_as_int(ay[1] * az[0]),
+                               __float_as_int(ay[0] * az[1]), __float_as_int(ay[1] * az[1]));
+        mine_at[5] = make_int4(__float_as_int(ax[0] * az[0]), __float_as_int(ax[1] * az[0]),
+                               __float_as_int(ax[0] * az[1]), __float_as_int(ax[1] * az[1]));
+        mine_at[6] = make_int4(__float_as_int(ax[0] * ay[0]), __float_as_int(ax[1] * ay[0]),
+                               __float_as_int(ax[0] * ay[1]), __float_as_int(ax[1] * ay[1]));
+        mine_at[7] = make_int4((int)mine.slow, mine.cx, mine.cy, mine.cz);
+      }
       const bool own = p0 + sub < g.P;
       // the point's rank in its bin: the K pass puts its entry at bin start + rank (the
       // returning atomic's latency is covered by the chunk's corner loads)
@@ -406,22 +433,51 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
       const int nk = min(L, g.P - p0);
       float4 rec = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       for (int kk = 0; kk < nk; ++kk) {
-        const int src = (grp * L + kk) << 2;
-        Point pt;
-        fetch_point(mine, src, pt);
         uint4 vr[8];
-        load_shared_corners<LY::kRowBytes, false>(g, win, vb, vb, b, m, lane_off, mine, src,
-                                                  pt.vidx, nullptr, vr);
+        float w[8], gx[4], gy[4], gz[4];
+        if constexpr (!kSlots) {
+          const int src = (grp * L + kk) << 2;
+          Point pt;
+          fetch_point(mine, src, pt);
+          load_shared_corners<LY::kRowBytes, false>(g, win, vb, vb, b, m, lane_off, mine, src,
+                                                    pt.vidx, nullptr, vr);
+#pragma unroll
+          for (int c = 0; c < 8; ++c) w[c] = pt.w[c];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            gx[e] = pt.ay[e & 1] * pt.az[e >> 1];
+            gy[e] = pt.ax[e & 1] * pt.az[e >> 1];
+            gz[e] = pt.ax[e & 1] * pt.ay[e >> 1];
+          }
+        } else {
+          const int4* at = pts[wave * 64 + grp * L + kk];
+          int vidx[8];
+          const int4 i0 = at[0], i1 = at[1];
+          vidx[0] = i0.x; vidx[1] = i0.y; vidx[2] = i0.z; vidx[3] = i0.w;
+          vidx[4] = i1.x; vidx[5] = i1.y; vidx[6] = i1.z; vidx[7] = i1.w;
+          load_stashed_corners<LY::kRowBytes, false>(g, win, vb, vb, b, m, lane_off, at + 7,
+                                                     vidx, nullptr, vr);
+          const int4 w0 = at[2], w1 = at[3], x4 = at[4], y4 = at[5], z4 = at[6];
+          w[0] = __int_as_float(w0.x); w[1] = __int_as_float(w0.y);
+          w[2] = __int_as_float(w0.z); w[3] = __int_as_float(w0.w);
+          w[4] = __int_as_float(w1.x); w[5] = __int_as_float(w1.y);
+          w[6] = __int_as_float(w1.z); w[7] = __int_as_float(w1.w);
+          gx[0] = __int_as_float(x4.x); gx[1] = __int_as_float(x4.y);
+          gx[2] = __int_as_float(x4.z); gx[3] = __int_as_float(x4.w);
+          gy[0] = __int_as_float(y4.x); gy[1] = __int_as_float(y4.y);
+          gy[2] = __int_as_float(y4.z); gy[3] = __int_as_float(y4.w);
+          gz[0] = __int_as_float(z4.x); gz[1] = __int_as_float(z4.y);
+          gz[2] = __int_as_float(z4.z); gz[3] = __int_as_float(z4.w);
+        }
         float dap = 0.0f, b3[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
+          const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
           const float dvv = chunk_dot<BF16>(gr, vr[c]);
-          float wx, wy, wz;
-          weight_grad(pt, c, wx, wy, wz);
-          dap = fmaf(pt.w[c], dvv, dap);
-          b3[0] = fmaf(wx, dvv, b3[0]);
-          b3[1] = fmaf(wy, dvv, b3[1]);
-          b3[2] = fmaf(wz, dvv, b3[2]);
+          dap = fmaf(w[c], dvv, dap);
+          b3[0] = fmaf(cx ? gx[c >> 1] : -gx[c >> 1], dvv, b3[0]);
+          b3[1] = fmaf(cy ? gy[cx + 2 * cz] : -gy[cx + 2 * cz], dvv, b3[1]);
+          b3[2] = fmaf(cz ? gz[c & 3] : -gz[c & 3], dvv, b3[2]);
         }
         const float da = group_sum<L>(dap);
 #pragma unroll
