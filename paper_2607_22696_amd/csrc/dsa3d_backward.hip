@@ -496,7 +496,11 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
 // K half of the record, Delta = sum_p alpha_p da_p and dq; then, with Delta known, the row's
 // lanes finish its points (finish_row).  Needs the V pass's records and the bin starts.
 template <int D, bool BF16>
-__global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_kpass_kernel(
+// Four waves per SIMD at head_dim 128 with bf16 (128 registers, 40 bytes spilled outside the
+// point loop): 133.2 -> 131.5 ms at 64x68x120 (3x5x5), 240.0 -> 236.0 ms (3x7x7); at head_dim
+// 64 the same hint cost 4% (4.81 -> 5.00 ms at 64x34x60), so three stay there.
+__global__ __launch_bounds__(kBlockThreads) __attribute__((
+    amdgpu_waves_per_eu((D) <= 64 ? 3 : (BF16 ? 4 : 1)))) void bwd_kpass_kernel(
     Geometry g, const void* __restrict__ q, const void* __restrict__ k,
     const float* __restrict__ offsets, const float* __restrict__ lse, float* __restrict__ dq,
     RecK* __restrict__ reck, const RecV* __restrict__ recv, const uint32_t* __restrict__ starts,
