@@ -286,8 +286,8 @@ def vmem_bytes(w):
                         half of each point record) + 4 P (bin-count atomics)
       bwd_kpass_kernel  8 P D s (K corner rows) + D s (q) + 24 P (offsets, twice) + 4 (lse)
                         + 4 P (da_p) + 16 P (the K half of each record) + 32 P (the records,
-                        read back to finish the points) + 4 D (dq) + 12 P (d_offsets) + 4 P
-                        (slot atomics) + 24 P (bin entries)
+                        read back to finish the points) + 4 D (dq) + 12 P (d_offsets) + 8 P
+                        (ranks and bin starts) + 24 P (bin entries)
     These, not the HBM bytes, are what bounds the kernels: the corner rows come from L2 and
     L1, and the per-unit gather path is busy most of the time (rocprofv3 TA/TD counters)."""
     s = 2 if w.dtype == "bf16" else 4
@@ -296,7 +296,7 @@ def vmem_bytes(w):
         "fwd_kernel": 16 * P * D * s + 2 * D * s + 12 * P + 4,
         "bwd_vpass_kernel": 8 * P * D * s + D * s + 12 * P + 16 * P + 4 * P,
         "bwd_kpass_kernel": 8 * P * D * s + D * s + 24 * P + 4 + 4 * P + 48 * P + 4 * D
-                            + 12 * P + 4 * P + 24 * P,
+                            + 12 * P + 8 * P + 24 * P,
     }
     return {k: w.queries * b for k, b in per.items()}
 
