@@ -346,15 +346,6 @@ __device__ inline __attribute__((always_inline)) void fetch_point(const Point& m
   for (int c = 0; c < 8; ++c) pt.w[c] = pt.ax[c & 1] * wyz[c >> 1];
 }
 
-// d w_c / d pos of corner c along x, y, z.
-__device__ inline __attribute__((always_inline)) void weight_grad(const Point& pt, int c,
-                                                                  float& wx, float& wy, float& wz) {
-  const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
-  wx = cx ? pt.ay[cy] * pt.az[cz] : -(pt.ay[cy] * pt.az[cz]);
-  wy = cy ? pt.ax[cx] * pt.az[cz] : -(pt.ax[cx] * pt.az[cz]);
-  wz = cz ? pt.ax[cx] * pt.ay[cy] : -(pt.ax[cx] * pt.ay[cy]);
-}
-
 // V pass: per point da_p = <dout, v_p> and B_p = sum_c dw_c/dpos <dout, V_c> into the V half
 // of the record; every point is counted into the bin of its cell.
 template <int D, bool BF16>
