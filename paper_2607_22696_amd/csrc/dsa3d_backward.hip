@@ -370,8 +370,8 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
   // fetch indices and fractions with ds_bpermute and rebuild the rest, which measured faster
   // there (2.98 against 3.10 ms at 64x34x60; 88.7 against 87.2 ms at 64x68x120, head_dim 128).
   constexpr bool kSlots = L >= 16;
-  __shared__ int4 pts[kSlots ? kBlockThreads : 1][8];
-  int4* const mine_at = pts[kSlots ? threadIdx.x : 0];
+  __shared__ int4 pts[kSlots ? slot_words<L, 9>() : 1];  // 8 words used, 9 for the banks
+  int4* const mine_at = pts + (kSlots ? slot_of<L, 9>(threadIdx.x) : 0);
 
   for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
     PencilTile tl;
@@ -441,7 +441,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
             gz[e] = pt.ax[e & 1] * pt.ay[e >> 1];
           }
         } else {
-          const int4* at = pts[wave * 64 + grp * L + kk];
+          const int4* at = pts + slot_of<L, 9>(wave * 64 + grp * L) + kk * 9;
           int vidx[8];
           const int4 i0 = at[0], i1 = at[1];
           vidx[0] = i0.x; vidx[1] = i0.y; vidx[2] = i0.z; vidx[3] = i0.w;
@@ -513,8 +513,8 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((
   // magnitudes of the weights' position derivatives (the products of two axis weights),
   // window flag and cell, and the point's da_p.  The owner forms them once instead of every
   // lane of the row rebuilding them, which the VALU-bound point loop feels.
-  __shared__ int4 pts[kBlockThreads][9];
-  int4* const mine_at = pts[threadIdx.x];
+  __shared__ int4 pts[slot_words<L, 9>()];
+  int4* const mine_at = pts + slot_of<L, 9>(threadIdx.x);
 
   for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
     PencilTile tl;
@@ -574,7 +574,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((
       const int nk = min(L, g.P - p0);
       float4 rec = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       for (int kk = 0; kk < nk; ++kk) {
-        const int4* at = pts[wave * 64 + grp * L + kk];
+        const int4* at = pts + slot_of<L, 9>(wave * 64 + grp * L) + kk * 9;
         int vidx[8];
         {
           const int4 i0 = at[0], i1 = at[1];

@@ -316,6 +316,23 @@ __device__ inline __attribute__((always_inline)) void load_stashed_corners(
   }
 }
 
+// LDS point slots: thread t of a block keeps N int4 (16-byte) words at slot_of<L, N>(t), with
+// one word of padding after each row's L slots.  The rows of a wave read one slot each in the
+// same instruction (the row's lanes read the same words: a broadcast); without the padding
+// their addresses would differ by L N 16 bytes, a multiple of the 256 bytes the LDS banks span
+// at L = 16, so all of them would hit the same banks.  With it they differ by L N 16 + 16
+// bytes, which for the slot sizes used here (N = 5 and 9, L = 8, 16 or 32) puts each row on a
+// different 16-byte bank group; an odd N keeps the writes of consecutive lanes, N 16 bytes
+// apart, on different bank groups too.
+template <int L, int N>
+__device__ inline __attribute__((always_inline)) int slot_of(int t) {
+  return t * N + t / L;
+}
+template <int L, int N>
+constexpr int slot_words() {
+  return kBlockThreads * N + kBlockThreads / L;
+}
+
 // ---------------------------------------------------------------------------- launch shape
 
 constexpr int kMaxBlocks = 1 << 22;  // grid cap; larger problems loop over tiles

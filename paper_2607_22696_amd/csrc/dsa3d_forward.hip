@@ -50,8 +50,8 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
   // The point each lane formed for the current chunk, read back by its row's lanes: corner
   // indices, weights, and for the global-load path its window flag and cell.  A row's lanes
   // are in one wave, whose LDS accesses complete in order: no barrier.
-  __shared__ int4 pts[kBlockThreads][5];
-  int4* const mine_at = pts[threadIdx.x];
+  __shared__ int4 pts[slot_words<L, 5>()];
+  int4* const mine_at = pts + slot_of<L, 5>(threadIdx.x);
 
   for (int64_t vt = blockIdx.x; vt < po.vtiles; vt += gridDim.x) {
     PencilTile tl;
@@ -97,7 +97,7 @@ __global__ __launch_bounds__(kBlockThreads) void fwd_kernel(
       const int nk = min(L, g.P - p0);
       for (int kk = 0; kk < nk; ++kk) {
         const int src = (grp * L + kk) << 2;
-        const int4* at = pts[wave * 64 + grp * L + kk];
+        const int4* at = pts + slot_of<L, 5>(wave * 64 + grp * L) + kk * 5;
         const int4 i0 = at[0], i1 = at[1], w0 = at[2], w1 = at[3];
         Point pt;
         pt.vidx[0] = i0.x; pt.vidx[1] = i0.y; pt.vidx[2] = i0.z; pt.vidx[3] = i0.w;
