@@ -285,17 +285,21 @@ def vmem_bytes(w):
       bwd_vpass_kernel  8 P D s (V corner rows) + D s (dout) + 12 P (offsets) + 16 P (the V
                         half of each point record) + 4 P (bin-count atomics)
       bwd_kpass_kernel  8 P D s (K corner rows) + D s (q) + 24 P (offsets, twice) + 4 (lse)
-                        + 4 P (da_p) + 16 P (the K half of each record) + 32 P (the records,
-                        read back to finish the points) + 4 D (dq) + 12 P (d_offsets) + 8 P
-                        (ranks and bin starts) + 24 P (bin entries)
+                        + 4 P (da_p) + 16 P (the V half of each record, read to finish the
+                        points) + 32 P (the K half, written and read back, only for rows of
+                        more than 5 chunks of L = D s / 16 points, whose K halves the kernel
+                        cannot hold in registers) + 4 D (dq) + 12 P (d_offsets) + 8 P (ranks
+                        and bin starts) + 24 P (bin entries)
     These, not the HBM bytes, are what bounds the kernels: the corner rows come from L2 and
     L1, and the per-unit gather path is busy most of the time (rocprofv3 TA/TD counters)."""
     s = 2 if w.dtype == "bf16" else 4
     P, D = w.P, w.head_dim
+    lanes = D * s // 16
+    kept = 32 * P if -(-P // lanes) > 5 else 0
     per = {
         "fwd_kernel": 16 * P * D * s + 2 * D * s + 12 * P + 4,
         "bwd_vpass_kernel": 8 * P * D * s + D * s + 12 * P + 16 * P + 4 * P,
-        "bwd_kpass_kernel": 8 * P * D * s + D * s + 24 * P + 4 + 4 * P + 48 * P + 4 * D
+        "bwd_kpass_kernel": 8 * P * D * s + D * s + 24 * P + 4 + 4 * P + 16 * P + kept + 4 * D
                             + 12 * P + 8 * P + 24 * P,
     }
     return {k: w.queries * b for k, b in per.items()}

@@ -257,70 +257,124 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
 // Delta is known its lanes finish the row's points: d_offsets and the point's entry, placed
 // at its bin's start + its rank (what the finalize pass does in the one-sweep order).
 
-// The row's points once its Delta is known, kFinish per lane at a time so that their loads
-// (record halves, offsets, ranks) and then their bin-start lookups are in flight together:
+// The row's points once its Delta is known, NB per lane at a time so that their loads
+// (V record halves, offsets, ranks) and then their bin-start lookups are in flight together:
 // d_offsets of each point and its entry in the bin of its cell, at slot starts[cell] + rank
-// (the point's rank in its bin, from the V pass).  Lane `sub` takes points sub, sub + L, ...:
-// it wrote the K half of exactly these records, and program order makes its own stores
-// visible to its loads.  (t, i, j): the query token; n its index in the batch item; bh its
-// (batch, head) group; row its query row.
+// (the point's rank in its bin, from the V pass).  Lane `sub` takes the points sub + c L of
+// the row's chunks c; p[u] >= P marks a lane with no point in that chunk.  rk holds the K
+// halves of the records (alpha_p, A_p) of those points.  (t, i, j): the query token; n its
+// index in the batch item; bh its (batch, head) group.
 constexpr int kFinish = 4;
+// Chunks of a row whose K record halves the K pass holds in registers (4 VGPRs each): rows of
+// up to 80 points at head_dim 128 and 40 at 64 in bf16.
+constexpr int kHoldChunks = 5;
 
-template <int L>
-__device__ inline __attribute__((always_inline)) void finish_row(
-    const Geometry& g, const RecK* __restrict__ krow, const RecV* __restrict__ vrow,
-    const float* __restrict__ off, const uint32_t* __restrict__ rrow, float delta, int bh, int n,
-    int t, int i, int j, int sub, float* __restrict__ drow, const uint32_t* __restrict__ starts,
-    Entry* __restrict__ entries) {
+template <int NB>
+__device__ inline __attribute__((always_inline)) void finish_points(
+    const Geometry& g, const RecK (&rk)[NB], const int (&p)[NB],
+    const RecV* __restrict__ vrow, const float* __restrict__ off,
+    const uint32_t* __restrict__ rrow, float delta, int bh, int n, int t, int i, int j,
+    float* __restrict__ drow, const uint32_t* __restrict__ starts, Entry* __restrict__ entries) {
   const int rt = (g.kt - 1) / 2, rh = (g.kh - 1) / 2, rw = (g.kw - 1) / 2;
-  for (int p0 = sub; p0 < g.P; p0 += kFinish * L) {
-    RecK rk[kFinish];
-    RecV rv[kFinish];
-    float o[kFinish][3];
-    uint32_t rank[kFinish];
+  RecV rv[NB];
+  float o[NB][3];
+  uint32_t rank[NB];
 #pragma unroll
-    for (int u = 0; u < kFinish; ++u) {
-      const int p = min(p0 + u * L, g.P - 1);  // past the row's end: a repeat, not stored
-      rk[u] = krow[p];
-      rv[u] = vrow[p];
-      o[u][0] = off[3 * p];
-      o[u][1] = off[3 * p + 1];
-      o[u][2] = off[3 * p + 2];
-      rank[u] = rrow[p];
+  for (int u = 0; u < NB; ++u) {
+    const int q = min(p[u], g.P - 1);  // no point: a repeat, not stored
+    rv[u] = vrow[q];
+    o[u][0] = off[3 * q];
+    o[u][1] = off[3 * q + 1];
+    o[u][2] = off[3 * q + 2];
+    rank[u] = rrow[q];
+  }
+  int cx[NB], cy[NB], cz[NB];
+  float fx[NB], fy[NB], fz[NB];
+  uint32_t slot[NB];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
+    const int q = min(p[u], g.P - 1);
+    const int iw = q % g.kw, ih = (q / g.kw) % g.kh, it = q / (g.kw * g.kh);
+    axis((float)(j + iw - rw), o[u][0], g.W, cx[u], fx[u]);
+    axis((float)(i + ih - rh), o[u][1], g.H, cy[u], fy[u]);
+    axis((float)(t + it - rt), o[u][2], g.T, cz[u], fz[u]);
+    slot[u] = 0xffffffffu;
+    if (cell_inside(g, cx[u], cy[u], cz[u]))
+      slot[u] = starts[cell_index(g, bh, cx[u], cy[u], cz[u])] + rank[u];
+  }
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
+    if (p[u] >= g.P) continue;
+    const float dd = rv[u].dalpha - delta;
+    const float sa = g.scale * dd;
+    float* d = drow + 3 * p[u];
+    d[0] = rk[u].alpha * fmaf(sa, rk[u].ax, rv[u].bx);
+    d[1] = rk[u].alpha * fmaf(sa, rk[u].ay, rv[u].by);
+    d[2] = rk[u].alpha * fmaf(sa, rk[u].az, rv[u].bz);
+    if (slot[u] == 0xffffffffu) continue;
+    Entry e;
+    e.n = (int32_t)n;
+    e.alpha = rk[u].alpha;
+    e.sds = g.scale * rk[u].alpha * dd;
+    e.fx = fx[u];
+    e.fy = fy[u];
+    e.fz = fz[u];
+    entries[slot[u]] = e;
+  }
+}
+
+// All of a row's points.  HOLD > 0: the lane kept the K halves of its points of the row's
+// (at most HOLD) chunks in registers, the latest chunk first (hold[h] is chunk nch - 1 - h);
+// it finishes them two at a time at 16 or more lanes per row, where the kernel has 128
+// registers (four at a time: 129.3 against 127.0 ms at 64x68x120, 3x5x5, head_dim 128, on
+// one box).
+// HOLD == 0: it stored them in the row's records (krow), and program order makes its own
+// stores visible to its loads.
+template <int L, int HOLD>
+__device__ inline __attribute__((always_inline)) void finish_row(
+    const Geometry& g, const RecK* __restrict__ krow, const float4 (&hold)[HOLD > 0 ? HOLD : 1],
+    const RecV* __restrict__ vrow, const float* __restrict__ off,
+    const uint32_t* __restrict__ rrow, float delta, int bh, int n, int t, int i, int j, int sub,
+    float* __restrict__ drow, const uint32_t* __restrict__ starts, Entry* __restrict__ entries) {
+  const int nch = (g.P + L - 1) / L;
+  // The points' index arithmetic depends only on the lane and the geometry: left visible, the
+  // compiler hoists it out of the tile loop for every held chunk and spills it there.
+  asm volatile("" : "+v"(sub));
+  if constexpr (HOLD > 0) {
+    // NB held points per batch of kFinish slots, the other slots empty (p = P): as a batch of
+    // two the compiler spills more (125.6 against 123.7 ms at 64x68x120, 3x5x5, head_dim 128)
+    constexpr int NB = L >= 16 ? 2 : kFinish;
+#pragma unroll
+    for (int h0 = 0; h0 < HOLD; h0 += NB) {
+      if (h0 >= nch) break;
+      int p[kFinish];
+      RecK rk[kFinish];
+#pragma unroll
+      for (int u = 0; u < kFinish; ++u) {
+        if (u >= NB) {
+          p[u] = g.P;
+          rk[u] = RecK{0.0f, 0.0f, 0.0f, 0.0f};
+          continue;
+        }
+        const int c = nch - 1 - (h0 + u);
+        p[u] = c >= 0 ? sub + c * L : g.P;
+        const float4 r = hold[h0 + u < HOLD ? h0 + u : HOLD - 1];
+        rk[u] = RecK{r.x, r.y, r.z, r.w};
+      }
+      finish_points<kFinish>(g, rk, p, vrow, off, rrow, delta, bh, n, t, i, j, drow, starts,
+                             entries);
     }
-    int cx[kFinish], cy[kFinish], cz[kFinish];
-    float fx[kFinish], fy[kFinish], fz[kFinish];
-    uint32_t slot[kFinish];
+  } else {
+    for (int c0 = 0; c0 < nch; c0 += kFinish) {
+      int p[kFinish];
+      RecK rk[kFinish];
 #pragma unroll
-    for (int u = 0; u < kFinish; ++u) {
-      const int p = min(p0 + u * L, g.P - 1);
-      const int iw = p % g.kw, ih = (p / g.kw) % g.kh, it = p / (g.kw * g.kh);
-      axis((float)(j + iw - rw), o[u][0], g.W, cx[u], fx[u]);
-      axis((float)(i + ih - rh), o[u][1], g.H, cy[u], fy[u]);
-      axis((float)(t + it - rt), o[u][2], g.T, cz[u], fz[u]);
-      slot[u] = 0xffffffffu;
-      if (cell_inside(g, cx[u], cy[u], cz[u]))
-        slot[u] = starts[cell_index(g, bh, cx[u], cy[u], cz[u])] + rank[u];
-    }
-#pragma unroll
-    for (int u = 0; u < kFinish; ++u) {
-      const int p = p0 + u * L;
-      if (p >= g.P) break;
-      const float dd = rv[u].dalpha - delta;
-      const float sa = g.scale * dd;
-      float* d = drow + 3 * p;
-      d[0] = rk[u].alpha * fmaf(sa, rk[u].ax, rv[u].bx);
-      d[1] = rk[u].alpha * fmaf(sa, rk[u].ay, rv[u].by);
-      d[2] = rk[u].alpha * fmaf(sa, rk[u].az, rv[u].bz);
-      if (slot[u] == 0xffffffffu) continue;
-      Entry e;
-      e.n = (int32_t)n;
-      e.alpha = rk[u].alpha;
-      e.sds = g.scale * rk[u].alpha * dd;
-      e.fx = fx[u];
-      e.fy = fy[u];
-      e.fz = fz[u];
-      entries[slot[u]] = e;
+      for (int u = 0; u < kFinish; ++u) {
+        p[u] = sub + (c0 + u) * L;
+        rk[u] = krow[min(p[u], g.P - 1)];
+      }
+      finish_points<kFinish>(g, rk, p, vrow, off, rrow, delta, bh, n, t, i, j, drow, starts,
+                             entries);
     }
   }
 }
@@ -483,10 +537,14 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_vpass_k
   }
 }
 
-// K pass: alpha_p from the logit and the forward's LSE, A_p = sum_c dw_c/dpos <q, K_c> into the
-// K half of the record, Delta = sum_p alpha_p da_p and dq; then, with Delta known, the row's
-// lanes finish its points (finish_row).  Needs the V pass's records and the bin starts.
-template <int D, bool BF16>
+// K pass: alpha_p from the logit and the forward's LSE, A_p = sum_c dw_c/dpos <q, K_c> (the
+// K half of the point's record), Delta = sum_p alpha_p da_p and dq; then, with Delta known, the
+// row's lanes finish its points (finish_row).  Needs the V pass's records and the bin starts.
+// HOLD > 0 (rows of at most HOLD chunks of L points): each lane keeps the K halves of its
+// points in registers until the row's end; HOLD == 0: it writes them to the records and reads
+// them back.  Holding them measured 131.4 -> 127.0 ms at 64x68x120 (3x5x5, head_dim 128) and
+// 4.76 -> 4.37 ms at 64x34x60 (3x3x3, head_dim 64).
+template <int D, bool BF16, int HOLD>
 // Four waves per SIMD at head_dim 128 with bf16 (128 registers, 40 bytes spilled outside the
 // point loop): 133.2 -> 131.5 ms at 64x68x120 (3x5x5), 240.0 -> 236.0 ms (3x7x7); at head_dim
 // 64 the same hint cost 4% (4.81 -> 5.00 ms at 64x34x60), so three stay there.
@@ -539,6 +597,9 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((
       bk[x] = 0.0f;
     }
     float delta = 0.0f;
+    float4 hold[HOLD > 0 ? HOLD : 1];
+#pragma unroll
+    for (int h = 0; h < (HOLD > 0 ? HOLD : 1); ++h) hold[h] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     int pm = min(sub, g.P - 1);
     float ox = off[3 * pm], oy = off[3 * pm + 1], oz = off[3 * pm + 2];
     for (int p0 = 0; p0 < g.P; p0 += L) {
@@ -626,7 +687,13 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((
         for (int a = 0; a < 3; ++a) a3[a] = group_sum<L>(a3[a]);
         if (sub == kk) rec = make_float4(alpha, a3[0], a3[1], a3[2]);
       }
-      if (own) *reinterpret_cast<float4*>(krow + p0 + sub) = rec;
+      if constexpr (HOLD > 0) {
+#pragma unroll
+        for (int h = HOLD - 1; h > 0; --h) hold[h] = hold[h - 1];
+        hold[0] = rec;
+      } else {
+        if (own) *reinterpret_cast<float4*>(krow + p0 + sub) = rec;
+      }
     }
     float* dqr = dq + row * D + sub * VEC;
 #pragma unroll
@@ -636,8 +703,8 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((
                       g.scale * fmaf(-delta, bk[x + 2], ak[x + 2]),
                       g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
     // Delta is known: finish the row's points
-    finish_row<L>(g, krow, vrow, off, ranks + row * g.P, delta, bh, n, t, i, j, sub,
-                  doff + row * g.P * 3, starts, entries);
+    finish_row<L, HOLD>(g, krow, hold, vrow, off, ranks + row * g.P, delta, bh, n, t, i, j, sub,
+                        doff + row * g.P * 3, starts, entries);
   }
 }
 
@@ -1391,8 +1458,11 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
     void* a[] = {(void*)&g,    (void*)&q,       (void*)&k,       (void*)&off,
                  (void*)&lse,  (void*)&dq,      (void*)&w.reck,  (void*)&w.recv, (void*)&w.starts,
                  (void*)&w.ranks, (void*)&doff, (void*)&w.entries, (void*)&po};
-    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_kpass_kernel<D, BF16>), dim3(blocks),
-                        dim3(kBlockThreads), a, 0, s);
+    constexpr int L = Layout<D, BF16>::kLanes;
+    const void* kern = (g.P + L - 1) / L <= kHoldChunks
+                           ? reinterpret_cast<const void*>(&bwd_kpass_kernel<D, BF16, kHoldChunks>)
+                           : reinterpret_cast<const void*>(&bwd_kpass_kernel<D, BF16, 0>);
+    e = hipLaunchKernel(kern, dim3(blocks), dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   } else {
     const int npoints = (int)points;

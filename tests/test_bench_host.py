@@ -57,6 +57,15 @@ def test_algorithmic_counts_follow_the_documented_per_row_formulas():
     assert alg["backward"]["flops"] == rows * 80 * P * D
     vm = bench.vmem_bytes(w)
     assert vm["fwd_kernel"] == rows * (16 * P * D * s + 2 * D * s + 12 * P + 4)
+    # the K pass keeps the K halves of the records in registers for rows of at most 5 chunks
+    # of D s / 16 points (here 4 chunks of 8), and writes and reads them back beyond that
+    kpass = 8 * P * D * s + D * s + 24 * P + 4 + 4 * P + 16 * P + 4 * D + 12 * P + 8 * P + 24 * P
+    assert vm["bwd_kpass_kernel"] == rows * kpass
+    w7 = testgen.WORKLOADS["paper_3x7x7_64x68x120"]  # P = 147, D = 128, bf16: 10 chunks of 16
+    P7, D7 = w7.P, w7.head_dim
+    kpass7 = (8 * P7 * D7 * 2 + D7 * 2 + 24 * P7 + 4 + 4 * P7 + 16 * P7 + 32 * P7 + 4 * D7
+              + 12 * P7 + 8 * P7 + 24 * P7)
+    assert bench.vmem_bytes(w7)["bwd_kpass_kernel"] == w7.queries * kpass7
 
 
 def test_more_than_one_gpu_is_refused_with_a_message():
