@@ -127,6 +127,17 @@ SMALL_CASES = [
           dtype="bf16", seed=28, offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
     small("k579_bf16_d64", T=5, H=7, W=9, heads=2, head_dim=64, kt=5, kh=7, kw=9, dtype="bf16",
           seed=29),
+    # the K pass holds a row's (alpha_p, A_p) in registers up to 5 chunks of L = D s / 16
+    # points and goes through the records beyond: 5 chunks of 8 with a ragged last one, 6 of 8,
+    # 6 of 16 (the chunk after 3x5x5's five), 4 of 4
+    small("k157_bf16_d64", T=4, H=7, W=9, heads=2, head_dim=64, kt=1, kh=5, kw=7, dtype="bf16",
+          seed=53),
+    small("k335_bf16_d64", T=4, H=6, W=7, heads=2, head_dim=64, kt=3, kh=3, kw=5, dtype="bf16",
+          seed=54),
+    small("k339_bf16_d128", T=4, H=6, W=11, heads=2, head_dim=128, kt=3, kh=3, kw=9,
+          dtype="bf16", seed=55, offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
+    small("k135_bf16_d32", T=3, H=6, W=7, heads=2, head_dim=32, kt=1, kh=3, kw=5, dtype="bf16",
+          seed=56),
     # grids thinner than one 4 x 2 x 2 gather block (a block with 2-4 cell columns, no second
     # row or plane)
     small("thin_bf16_d64", T=3, H=1, W=3, heads=2, head_dim=64, dtype="bf16", seed=50),
