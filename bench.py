@@ -321,8 +321,8 @@ def gather_ceiling(row_bytes):
     """The gather microbenchmark (libgather_probe.so): 16-byte lane loads, one contiguous row
     of row_bytes per lane group at pseudo-random addresses, every row already in L1 (the
     ceiling of the kernels' gather path), every row missing L1 and hitting L2, the same
-    pattern from LDS, and rows from a 512 MB region (missing L2: what comes from past the
-    L2s)."""
+    pattern from LDS, rows from a 512 MB region (missing L2: what comes from past the L2s),
+    and the L1- and L2-resident rows through direct-to-LDS loads."""
     import ctypes
     if not os.path.exists(PROBE_LIB):
         raise RuntimeError(f"{PROBE_LIB} is missing: build it with __graft_entry__.build()")
@@ -331,7 +331,8 @@ def gather_ceiling(row_bytes):
                                        ctypes.POINTER(ctypes.c_float),
                                        ctypes.POINTER(ctypes.c_double)]
     out = {"row_bytes": row_bytes}
-    for src, name in ((0, "l1"), (2, "l2"), (1, "lds"), (3, "mem")):
+    for src, name in ((0, "l1"), (2, "l2"), (1, "lds"), (3, "mem"), (4, "l1_to_lds"),
+                      (5, "l2_to_lds")):
         ms, nb = ctypes.c_float(), ctypes.c_double()
         rc = lib.dsa3d_probe_gather(src, row_bytes, 2048, 4096, ctypes.byref(ms), ctypes.byref(nb))
         if rc != 0:

@@ -84,7 +84,8 @@ def test_gather_probe_rejects_bad_arguments_before_touching_the_device():
     fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]
     ms, nb = ctypes.c_float(), ctypes.c_double()
-    assert fn(4, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no such source
+    assert fn(6, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no such source
+    assert fn(4, 128, 8, 12, ctypes.byref(ms), ctypes.byref(nb)) == -1  # not 8 loads a step
     assert fn(-1, 128, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1
     assert fn(2, 48, 8, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1    # row size
     assert fn(0, 128, 0, 8, ctypes.byref(ms), ctypes.byref(nb)) == -1   # no blocks
