@@ -19,7 +19,9 @@
 //       dq = scale (sum_p alpha_p da_p k_p - Delta sum_p alpha_p k_p);
 //     then the row's lanes finish its points: d_offsets[p] = alpha_p (scale (da_p - Delta) A_p
 //     + B_p), and the point's dK/dV coefficients (scale ds_p, alpha_p) and fractional position
-//     go to slot bin start + rank, i.e. sorted by cell.
+//     go to slot bin start + rank, i.e. sorted by cell.  (alpha_p, A_p) wait for the row's end
+//     in registers when the row has at most kHoldChunks chunks of L points, else in the K
+//     half of the point's record.
 //  4. gather: a voxel is corner c of exactly the points whose cell is voxel - c, so a block
 //     of voxels reads the bins of the cells around it, a few runs of adjacent bins, and
 //     stores the dK and dV rows of its voxels once.  bf16: one wave per 4 x 2 x 2 block, the
