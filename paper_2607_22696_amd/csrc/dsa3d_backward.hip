@@ -83,29 +83,25 @@ __device__ inline bool cell_inside(const Geometry& g, int x, int y, int z) {
 
 // ---------------------------------------------------------------------------- 1. sweep
 
+// The predicted-weights variant's sweep (the logit of a point is given, `logits`, so q and the
+// K corners are not read and there is no dq; the main operator's V and K passes are below).
 // The lanes of a row share each point's coordinate work: in a chunk of L points, lane `sub`
 // forms point chunk + sub (position, corners, weights, cell), counts it into its bin, and
 // the row's lanes pick the corner indices, fractions and cell up with ds_bpermute; the
 // weights are rebuilt from the fractions with the same products.  Lane `sub` also keeps
-// that point's record, and the row stores the chunk's records as one contiguous block.
-//
-// PW (the predicted-weights variant): the logit of a point is given (`logits`), so q and the K
-// corners are not read, there is no dq, and A_p = 0 in the record.
-template <int D, bool BF16, bool PW>
+// that point's record (alpha_p and A_p = 0; da_p and B_p), and the row stores the chunk's
+// records as one contiguous block.
+template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_kernel(
-    Geometry g, const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
-    const float* __restrict__ logits, const float* __restrict__ offsets,
-    const float* __restrict__ lse, const void* __restrict__ dout, float* __restrict__ dq,
-    RecK* __restrict__ reck, RecV* __restrict__ recv, float* __restrict__ delta_out,
-    uint32_t* __restrict__ counts, PencilOrder po) {
+    Geometry g, const void* __restrict__ v, const float* __restrict__ logits,
+    const float* __restrict__ offsets, const float* __restrict__ lse,
+    const void* __restrict__ dout, RecK* __restrict__ reck, RecV* __restrict__ recv,
+    float* __restrict__ delta_out, uint32_t* __restrict__ counts, PencilOrder po) {
   using LY = Layout<D, BF16>;
   constexpr int L = LY::kLanes;
-  constexpr int VEC = LY::kVec;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / L, sub = lane % L;
   const int lane_off = sub * 16;
-  const char* qb = static_cast<const char*>(q);
-  const char* kb = static_cast<const char*>(k);
   const char* vb = static_cast<const char*>(v);
   const char* gb = static_cast<const char*>(dout);
   const int HW = g.H * g.W;
@@ -118,7 +114,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
     const int bh = tl.group;
     const int b = bh / g.heads, m = bh % g.heads;
     const int t = tl.frame;
-    const RowWindow win = make_window<LY::kRowBytes>(g, k, v, b, m, t);
+    const RowWindow win = make_window<LY::kRowBytes>(g, v, v, b, m, t);  // V rows only
     int i, j;
     // All lanes of a group share the token: a whole group is idle or active, so neither the
     // group reductions nor the point sharing ever mix an idle group into an active one.
@@ -126,17 +122,9 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
     const int n = t * HW + i * g.W + j;
     const int64_t row = ((int64_t)b * g.N + n) * g.heads + m;
 
-    uint4 qr = make_uint4(0u, 0u, 0u, 0u);
-    if constexpr (!PW) qr = load16(qb, row * LY::kRowBytes + lane_off);
     const uint4 gr = load16(gb, row * LY::kRowBytes + lane_off);
     const float lse2 = lse[row] * kLog2e;
     const float* off = offsets + row * g.P * 3;
-    float ak[VEC], bk[VEC];
-#pragma unroll
-    for (int x = 0; x < VEC; ++x) {
-      ak[x] = 0.0f;
-      bk[x] = 0.0f;
-    }
     float delta = 0.0f;
 
     int pm = min(sub, g.P - 1);  // this lane's point of the chunk (clamped in the last one)
@@ -145,8 +133,7 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
       const int it = pm / khw, ih = (pm - it * khw) / g.kw, iw = pm - it * khw - ih * g.kw;
       Point mine;
       make_point(g, win, t, i, j, it - rt, ih - rh, iw - rw, ox, oy, oz, mine);
-      float mylog2 = 0.0f;  // PW: this lane's point's logit, base 2
-      if constexpr (PW) mylog2 = logits[row * g.P + pm] * kLog2e;
+      const float mylog2 = logits[row * g.P + pm] * kLog2e;  // this lane's point's logit, base 2
       const bool own = p0 + sub < g.P;
       if (own && cell_inside(g, mine.cx, mine.cy, mine.cz))  // result unused: no wait
         __hip_atomic_fetch_add(counts + cell_index(g, bh, mine.cx, mine.cy, mine.cz), 1u,
@@ -177,14 +164,10 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
 #pragma unroll
           for (int c = 0; c < 8; ++c) pt.w[c] = pt.ax[c & 1] * wyz[c >> 1];
         }
-        uint4 kr[8], vr[8];
-        load_shared_corners<LY::kRowBytes, !PW>(g, win, kb, vb, b, m, lane_off, mine, src,
-                                                pt.vidx, kr, vr);
-        float sp = 0.0f, dap = 0.0f;
-        float a3[3] = {0.0f, 0.0f, 0.0f}, b3[3] = {0.0f, 0.0f, 0.0f};
-        float kp[VEC];
-#pragma unroll
-        for (int x = 0; x < VEC; ++x) kp[x] = 0.0f;
+        uint4 vr[8];
+        load_shared_corners<LY::kRowBytes, false>(g, win, vb, vb, b, m, lane_off, mine, src,
+                                                  pt.vidx, nullptr, vr);
+        float dap = 0.0f, b3[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
           const int cx = c & 1, cy = (c >> 1) & 1, cz = c >> 2;
@@ -197,38 +180,15 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
           b3[0] = fmaf(wx, dvv, b3[0]);
           b3[1] = fmaf(wy, dvv, b3[1]);
           b3[2] = fmaf(wz, dvv, b3[2]);
-          if constexpr (!PW) {
-            const float qk = chunk_dot<BF16>(qr, kr[c]);
-            sp = fmaf(pt.w[c], qk, sp);
-            a3[0] = fmaf(wx, qk, a3[0]);
-            a3[1] = fmaf(wy, qk, a3[1]);
-            a3[2] = fmaf(wz, qk, a3[2]);
-            chunk_axpy<BF16>(kp, pt.w[c], kr[c]);
-          }
         }
-        float alpha;
-        if constexpr (PW)
-          alpha = exp2f(__int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mylog2))) -
-                        lse2);
-        else
-          alpha = exp2f(group_sum<L>(sp) * g.scale_log2 - lse2);
+        const float alpha =
+            exp2f(__int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mylog2))) - lse2);
         const float da = group_sum<L>(dap);
         delta = fmaf(alpha, da, delta);
-        if constexpr (!PW) {
-          const float ada = alpha * da;
 #pragma unroll
-          for (int x = 0; x < VEC; ++x) {
-            ak[x] = fmaf(ada, kp[x], ak[x]);
-            bk[x] = fmaf(alpha, kp[x], bk[x]);
-          }
-        }
-#pragma unroll
-        for (int a = 0; a < 3; ++a) {
-          if constexpr (!PW) a3[a] = group_sum<L>(a3[a]);
-          b3[a] = group_sum<L>(b3[a]);
-        }
+        for (int a = 0; a < 3; ++a) b3[a] = group_sum<L>(b3[a]);
         if (sub == kk) {
-          rec0 = make_float4(alpha, a3[0], a3[1], a3[2]);
+          rec0 = make_float4(alpha, 0.0f, 0.0f, 0.0f);
           rec1 = make_float4(da, b3[0], b3[1], b3[2]);
         }
       }
@@ -236,15 +196,6 @@ __global__ __launch_bounds__(kBlockThreads) DSA3D_WAVES_HINT(D) void bwd_sweep_k
         *reinterpret_cast<float4*>(reck + row * g.P + p0 + sub) = rec0;
         *reinterpret_cast<float4*>(recv + row * g.P + p0 + sub) = rec1;
       }
-    }
-    if constexpr (!PW) {
-      float* dqr = dq + row * D + sub * VEC;
-#pragma unroll
-      for (int x = 0; x < VEC; x += 4)
-        *reinterpret_cast<float4*>(dqr + x) =
-          make_float4(g.scale * fmaf(-delta, bk[x], ak[x]), g.scale * fmaf(-delta, bk[x + 1], ak[x + 1]),
-                      g.scale * fmaf(-delta, bk[x + 2], ak[x + 2]),
-                        g.scale * fmaf(-delta, bk[x + 3], ak[x + 3]));
     }
     if (sub == 0) delta_out[row] = delta;
   }
@@ -1429,13 +1380,11 @@ hipError_t bwd_dispatch(const Geometry& g, const void* q, const void* k, const v
                         dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   } else {
-    void* a[] = {(void*)&g,    (void*)&q,      (void*)&k,       (void*)&v,
-                 (void*)&logits, (void*)&off,  (void*)&lse,     (void*)&dout,
-                 (void*)&dq,   (void*)&w.reck, (void*)&w.recv, (void*)&w.delta, (void*)&w.counts,
-                 (void*)&po};
-    const void* kern = pw ? reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, true>)
-                          : reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16, false>);
-    e = hipLaunchKernel(kern, dim3(blocks), dim3(kBlockThreads), a, 0, s);
+    void* a[] = {(void*)&g,      (void*)&v,      (void*)&logits,  (void*)&off,
+                 (void*)&lse,    (void*)&dout,   (void*)&w.reck,  (void*)&w.recv,
+                 (void*)&w.delta, (void*)&w.counts, (void*)&po};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_sweep_kernel<D, BF16>), dim3(blocks),
+                        dim3(kBlockThreads), a, 0, s);
     if (e != hipSuccess) return e;
   }
   if ((e = mark(1)) != hipSuccess) return e;
