@@ -138,6 +138,11 @@ SMALL_CASES = [
           dtype="bf16", seed=55, offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
     small("k135_bf16_d32", T=3, H=6, W=7, heads=2, head_dim=32, kt=1, kh=3, kw=5, dtype="bf16",
           seed=56),
+    # fp32 rows take twice the lanes: 3 chunks of 32 (ragged), 5 of 16, 6 of 8
+    small("k355_f32_d128", T=3, H=5, W=6, heads=1, head_dim=128, kt=3, kh=5, kw=5, seed=57,
+          offsets=testgen.Dist(testgen.UNIFORM, -3.0, 3.0)),
+    small("k355_f32_d64", T=3, H=6, W=7, heads=2, head_dim=64, kt=3, kh=5, kw=5, seed=58),
+    small("k335_f32_d32", T=4, H=6, W=7, heads=2, head_dim=32, kt=3, kh=3, kw=5, seed=59),
     # grids thinner than one 4 x 2 x 2 gather block (a block with 2-4 cell columns, no second
     # row or plane)
     small("thin_bf16_d64", T=3, H=1, W=3, heads=2, head_dim=64, dtype="bf16", seed=50),
